@@ -1,0 +1,38 @@
+"""FP64 CPU oracle for the decoder-layer training hot path.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path (the HIP library and
+its Python binding) may import, call or link anything in this package.  Only
+the test-suite, the smoke check and the CPU-baseline leg of the benchmark use
+it.
+
+What it computes is the plain mathematical definition of each step, in
+float64, from the float16 input values (the paper states that its backend
+preserves the model computation exactly; Sec. 4.1 and Sec. 5.3):
+
+* ``gemm``       -- C = alpha * op(A) @ op(B) + beta * C           (Sec. 4.1, FP16 GEMM backend)
+* ``attention``  -- causal / GQA softmax attention forward and its
+                    gradient (Sec. 4.1, Algorithm 1, Memory-resident
+                    Attention Backward)
+* ``swiglu``     -- SwiGLU gate of the FFN projection and its gradient
+* ``layer``      -- one decoder layer forward + backward composed of the above
+
+No blocking, fusion, online softmax or reordering: a reader can check each
+function against the definitions by eye.  Library primitives used as single
+steps: numpy's float64 matmul, exp, log and reductions.
+
+Every function here is pinned by the CPU tests in ``tests/test_oracle_*.py``
+(brute force, closed forms, finite differences, invariants, hand-derived
+worked examples under ``tests/golden/``).
+"""
+
+from .gemm import gemm, gemm_entries
+from .attention import attn_fwd, attn_bwd, attn_head_fwd, attn_head_bwd
+from .swiglu import silu, swiglu_fwd, swiglu_bwd
+from .layer import LayerShape, layer_fwd, layer_bwd, layer_flops
+
+__all__ = [
+    "gemm", "gemm_entries",
+    "attn_fwd", "attn_bwd", "attn_head_fwd", "attn_head_bwd",
+    "silu", "swiglu_fwd", "swiglu_bwd",
+    "LayerShape", "layer_fwd", "layer_bwd", "layer_flops",
+]

@@ -1,0 +1,124 @@
+"""Oracle decoder layer forward + backward (test infrastructure only).
+
+Composition of the oracle steps into one dense decoder layer as used by the
+paper's workloads (decoder-only Transformer layers, Sec. 2.2 and Sec. 3.3;
+GEMM consumers QKV / output / FFN projections, Sec. 4.1; LLaMA-2, Baichuan2,
+Qwen2.5 shapes, Sec. 6.1).  The paper mentions no normalisation, rotary
+embedding, bias or dropout, so the layer here has none; the two residual
+additions are kept.
+
+Forward, X [T, H] with T = B*S rows (batch-major):
+    QKV = X Wqkv^T          Wqkv [(Hq + 2 Hkv) d, H]: Q heads, then K, then V
+    O, LSE = attention(Q, K, V)   per batch, causal
+    H1  = X + O Wo^T         Wo  [H, Hq d]
+    GU  = H1 Wgu^T           Wgu [2F, H]: gate rows, then up rows
+    A   = silu(G) * U
+    Y   = H1 + A Wd^T        Wd  [H, F]
+
+Backward of sum(Y * dY):
+    dWd = dY^T A ;  dA = dY Wd ;  dGU = swiglu_bwd(dA, GU)
+    dWgu = dGU^T H1 ;  dH1 = dY + dGU Wgu
+    dWo = dH1^T O ;  dO = dH1 Wo
+    dQ, dK, dV = attention_bwd(Q, K, V, dO) -> dQKV
+    dWqkv = dQKV^T X ;  dX = dH1 + dQKV Wqkv
+
+All intermediates stay float64 (no float16 rounding of intermediates).
+"""
+
+from dataclasses import dataclass
+
+import numpy as np
+
+from .attention import attn_fwd, attn_bwd
+from .swiglu import swiglu_fwd, swiglu_bwd
+
+
+@dataclass(frozen=True)
+class LayerShape:
+    B: int      # micro-batch
+    S: int      # sequence length
+    H: int      # hidden size
+    Hq: int     # query heads
+    Hkv: int    # key/value heads
+    D: int      # head dim
+    F: int      # FFN size
+
+    @property
+    def T(self):
+        return self.B * self.S
+
+    @property
+    def qkv_cols(self):
+        return (self.Hq + 2 * self.Hkv) * self.D
+
+
+def _split_qkv(qkv, sh):
+    """[T, (Hq+2Hkv)d] -> q [B,S,Hq,d], k, v [B,S,Hkv,d] (views)."""
+    qd = sh.Hq * sh.D
+    kd = sh.Hkv * sh.D
+    q = qkv[:, :qd].reshape(sh.B, sh.S, sh.Hq, sh.D)
+    k = qkv[:, qd:qd + kd].reshape(sh.B, sh.S, sh.Hkv, sh.D)
+    v = qkv[:, qd + kd:].reshape(sh.B, sh.S, sh.Hkv, sh.D)
+    return q, k, v
+
+
+def layer_fwd(sh, X, Wqkv, Wo, Wgu, Wd):
+    """Returns a dict of float64 activations including 'Y'."""
+    X = np.asarray(X, dtype=np.float64)
+    Wqkv, Wo, Wgu, Wd = (np.asarray(w, dtype=np.float64) for w in (Wqkv, Wo, Wgu, Wd))
+    scale = 1.0 / np.sqrt(sh.D)
+    qkv = X @ Wqkv.T
+    q, k, v = _split_qkv(qkv, sh)
+    o4, lse = attn_fwd(q, k, v, scale, causal=True)
+    O = o4.reshape(sh.T, sh.Hq * sh.D)
+    H1 = X + O @ Wo.T
+    GU = H1 @ Wgu.T
+    A = swiglu_fwd(GU)
+    Y = H1 + A @ Wd.T
+    return {"QKV": qkv, "O": O, "LSE": lse, "H1": H1, "GU": GU, "A": A, "Y": Y}
+
+
+def layer_bwd(sh, X, Wqkv, Wo, Wgu, Wd, dY, acts=None):
+    """Gradient of sum(Y * dY) w.r.t. X and the four weights (float64 dict)."""
+    X = np.asarray(X, dtype=np.float64)
+    Wqkv, Wo, Wgu, Wd = (np.asarray(w, dtype=np.float64) for w in (Wqkv, Wo, Wgu, Wd))
+    dY = np.asarray(dY, dtype=np.float64)
+    if acts is None:
+        acts = layer_fwd(sh, X, Wqkv, Wo, Wgu, Wd)
+    scale = 1.0 / np.sqrt(sh.D)
+    dWd = dY.T @ acts["A"]
+    dA = dY @ Wd
+    dGU = swiglu_bwd(dA, acts["GU"])
+    dWgu = dGU.T @ acts["H1"]
+    dH1 = dY + dGU @ Wgu
+    dWo = dH1.T @ acts["O"]
+    dO = dH1 @ Wo
+    q, k, v = _split_qkv(acts["QKV"], sh)
+    dq, dk, dv, _ = attn_bwd(q, k, v, dO.reshape(sh.B, sh.S, sh.Hq, sh.D), scale, causal=True)
+    dQKV = np.concatenate([dq.reshape(sh.T, -1), dk.reshape(sh.T, -1), dv.reshape(sh.T, -1)], axis=1)
+    dWqkv = dQKV.T @ X
+    dX = dH1 + dQKV @ Wqkv
+    return {"dX": dX, "dWqkv": dWqkv, "dWo": dWo, "dWgu": dWgu, "dWd": dWd,
+            "dA": dA, "dGU": dGU, "dH1": dH1, "dO": dO, "dQKV": dQKV}
+
+
+def layer_flops(sh):
+    """Algorithmic FLOPs (2 per multiply-add) of one layer forward + backward.
+
+    GEMMs: every weight is used by three products (fwd, dgrad, wgrad).
+    Attention counts only the causal triangle S(S+1)/2 of (i, j) pairs:
+    forward 2 contractions (QK^T, PV), backward the 4 contractions of
+    Algorithm 1 (GO V^T, P^T GO, GS K, GS^T Q); the score recomputation
+    of a recompute-P backward is not counted.
+    """
+    T = sh.T
+    # per weight [out, in]: forward product 2*T*out*in FLOPs
+    gemm_fwd = 2 * T * (sh.qkv_cols * sh.H          # Wqkv
+                        + sh.H * sh.Hq * sh.D       # Wo
+                        + 2 * sh.F * sh.H           # Wgu
+                        + sh.H * sh.F)              # Wd
+    pairs = sh.S * (sh.S + 1) // 2
+    attn_fwd_fl = 2 * 2 * sh.D * pairs * sh.Hq * sh.B
+    attn_bwd_fl = 4 * 2 * sh.D * pairs * sh.Hq * sh.B
+    return {"gemm": 3 * gemm_fwd, "attn_fwd": attn_fwd_fl, "attn_bwd": attn_bwd_fl,
+            "total": 3 * gemm_fwd + attn_fwd_fl + attn_bwd_fl}
