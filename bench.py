@@ -1,0 +1,206 @@
+#!/usr/bin/env python3
+"""Benchmark: one dense decoder layer forward + backward on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic input:
+the 12 layer GEMMs (fwd / dgrad / wgrad of QKV, O, gate/up and down), causal
+attention forward and backward, and the SwiGLU gate -- every step a liblt
+HIP launch on one stream, inputs resident in HBM before timing starts.
+
+Prints ONE JSON line.  ``value`` is the layer's algorithmic FLOP rate (GEMM
+FLOPs + attention forward over the causal triangle + the 4-contraction
+attention backward) divided by the measured step time.
+
+    python bench.py [--gpus 1] [--steps 10] [--warmup 3] [--workload llama2-7b]
+"""
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2606_10415_amd.synth import WORKLOADS, layer_inputs  # noqa: E402
+
+PEAK_FP16_TFLOPS = 2516.6     # MI355X dense FP16 MFMA (256 CU x 2.4 GHz x 4096 FLOP/clk)
+PEAK_HBM_GBS = 8000.0
+
+
+def layer_flops(w):
+    T = w.T
+    gemm_fwd = 2 * T * (w.qkv_cols * w.H + w.H * w.Hq * w.D + 2 * w.F * w.H + w.H * w.F)
+    pairs = w.S * (w.S + 1) // 2
+    attn_fwd = 2 * 2 * w.D * pairs * w.Hq * w.B
+    attn_bwd = 4 * 2 * w.D * pairs * w.Hq * w.B
+    return {"gemm": 3 * gemm_fwd, "attn_fwd": attn_fwd, "attn_bwd": attn_bwd,
+            "total": 3 * gemm_fwd + attn_fwd + attn_bwd}
+
+
+def cpu_baseline(w, budget_s=20.0):
+    """Time the float64 oracle on a bounded sample of the same workload.
+
+    Sample: the first R rows of every one of the 12 GEMMs (R chosen so the
+    sample takes a few seconds) plus one full attention head forward and
+    backward at the workload's sequence length.  Rate = algorithmic FLOPs of
+    the sample / wall time.
+    """
+    import oracle
+    from paper_2606_10415_amd.synth import normal_f16
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    T = w.T
+    R = 128
+    shapes = [(T, w.qkv_cols, w.H), (T, w.H, w.Hq * w.D), (T, 2 * w.F, w.H), (T, w.H, w.F),
+              (w.H, w.F, T), (T, w.F, w.H), (2 * w.F, w.H, T), (T, w.H, 2 * w.F),
+              (w.H, w.Hq * w.D, T), (T, w.Hq * w.D, w.H), (w.qkv_cols, w.H, T), (T, w.H, w.qkv_cols)]
+    flops = 0
+    t_total = 0.0
+    for i, (M, N, K) in enumerate(shapes):
+        a = normal_f16(90000 + i, (R, K))
+        b = normal_f16(90100 + i, (K, N), 0.02)
+        t0 = time.perf_counter()
+        oracle.gemm(0, 0, 1.0, a, b)
+        t_total += time.perf_counter() - t0
+        flops += 2 * R * N * K
+        if t_total > budget_s:
+            break
+    S, D = w.S, w.D
+    q = normal_f16(90200, (S, D)); k = normal_f16(90201, (S, D))
+    v = normal_f16(90202, (S, D)); do = normal_f16(90203, (S, D))
+    t0 = time.perf_counter()
+    oracle.attn_head_fwd(q, k, v, 1 / math.sqrt(D), True)
+    oracle.attn_head_bwd(q, k, v, do, 1 / math.sqrt(D), True)
+    t_total += time.perf_counter() - t0
+    pairs = S * (S + 1) // 2
+    flops += 6 * 2 * D * pairs
+    return {"value": flops / t_total / 1e12, "unit": "TFLOP/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": (f"{w.name}: first {R} rows of each of the 12 layer GEMMs + one full causal "
+                       f"attention head fwd+bwd (S={S}, d={D}); {flops / 1e9:.1f} GFLOP in "
+                       f"{t_total:.1f} s, float64 numpy/OpenBLAS")}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama2-7b", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU (its layer at full shape); --gpus {args.gpus} is not "
+              "supported: the data-parallel path needs no collective inside a layer step and "
+              "this build runs on one MI355X only", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a ROCm GPU"
+    from paper_2606_10415_amd.layer import DecoderLayer
+
+    w = WORKLOADS[args.workload]
+    print(f"[bench] workload {w.name}: generating inputs", file=sys.stderr, flush=True)
+    L = DecoderLayer(w, layer_inputs(w))
+    stream = torch.cuda.current_stream()
+    fl = layer_flops(w)
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        L.step()
+    torch.cuda.synchronize()
+
+    # timed region: events around every launch, on the stream the kernels run on
+    names_per_step = []
+    events = []
+
+    def hook(name):
+        ev = torch.cuda.Event(enable_timing=True)
+        ev.record(stream)
+        events.append((name, ev))
+
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record(stream)
+    for _ in range(args.steps):
+        hook("__step__")
+        L.step(hook=hook)
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_total = start.elapsed_time(end)
+    ms_per_step = ms_total / args.steps
+
+    per_op = {}
+    prev = None
+    for name, ev in events:
+        if prev is not None and name != "__step__":
+            per_op.setdefault(name, []).append(prev.elapsed_time(ev))
+        prev = ev
+    avg = {k: float(np.mean(v)) for k, v in per_op.items()}
+    gemm_names = [n for n, *_ in L.gemm_shapes()]
+    gemm_ms = sum(avg[n] for n in gemm_names)
+    gemm_tflops = fl["gemm"] / (gemm_ms * 1e-3) / 1e12
+    attn_bwd_tflops = fl["attn_bwd"] / (avg["attn_bwd"] * 1e-3) / 1e12
+    attn_fwd_tflops = fl["attn_fwd"] / (avg["attn_fwd"] * 1e-3) / 1e12
+    value = fl["total"] / (ms_per_step * 1e-3) / 1e12
+
+    detail = {
+        "gemm_ms": round(gemm_ms, 4), "gemm_tflops": round(gemm_tflops, 1),
+        "gemm_frac_peak": round(gemm_tflops / PEAK_FP16_TFLOPS, 4),
+        "attn_fwd_ms": round(avg["attn_fwd"], 4), "attn_fwd_tflops": round(attn_fwd_tflops, 1),
+        "attn_bwd_ms": round(avg["attn_bwd"], 4), "attn_bwd_tflops": round(attn_bwd_tflops, 1),
+        "attn_bwd_frac_peak": round(attn_bwd_tflops / PEAK_FP16_TFLOPS, 4),
+        "swiglu_fwd_ms": round(avg["swiglu_fwd"], 4), "swiglu_bwd_ms": round(avg["swiglu_bwd"], 4),
+        "swiglu_fwd_gbs": round(6 * w.T * w.F / (avg["swiglu_fwd"] * 1e-3) / 1e9, 1),
+        "swiglu_bwd_gbs": round(10 * w.T * w.F / (avg["swiglu_bwd"] * 1e-3) / 1e9, 1),
+        "per_op_ms": {k: round(v, 4) for k, v in avg.items()},
+        "wall_s": round(wall, 3),
+    }
+    print("[bench] " + json.dumps(detail), file=sys.stderr, flush=True)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle sample)", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w)
+
+    out = {
+        "metric": "decoder-layer fwd+bwd TFLOP/s (GEMM, attn-bwd) and % of FP16 MFMA peak",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic (seeded N(0,1) activations/grads, N(0,0.02^2) weights, fp16)",
+        "config": {"workload": f"{w.name} decoder layer fwd+bwd", "B": w.B, "S": w.S, "H": w.H,
+                   "Hq": w.Hq, "Hkv": w.Hkv, "D": w.D, "F": w.F, "causal": True,
+                   "flops_per_step": fl["total"], "parallelism": "single GPU"},
+        "frac_of_peak": round(value / PEAK_FP16_TFLOPS, 4),
+        "roofline": {"bound": "mfma", "kernel": "gemm_f16 (12 launches per step)",
+                     "achieved": round(gemm_tflops, 1), "peak": PEAK_FP16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK_FP16_TFLOPS, 4),
+                     "traffic": None},
+        "attn_bwd": {"achieved": round(attn_bwd_tflops, 1), "peak": PEAK_FP16_TFLOPS,
+                     "frac": round(attn_bwd_tflops / PEAK_FP16_TFLOPS, 4)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

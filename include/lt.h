@@ -1,0 +1,189 @@
+/*
+ * lt.h -- C ABI of the MI355X (gfx950) decoder-layer training kernels.
+ *
+ * The operations are the training-critical-path compute of one dense
+ * decoder layer as described in Sec. 4.1 of the paper: the FP16 GEMM
+ * primitive used by the QKV, output and FFN projections (forward, data
+ * gradient and weight gradient), causal multi-head / grouped-query
+ * attention forward, and the attention backward of Algorithm 1 (computed
+ * here with recomputed probabilities from a saved per-row log-sum-exp),
+ * plus the SwiGLU gate that joins the two FFN projections.
+ *
+ * General conventions
+ *   - lt_half is the bit pattern of an IEEE-754 binary16 value.
+ *   - All matrices are row-major.  "ld" / "row_stride" arguments are in
+ *     elements, not bytes.
+ *   - Every pointer argument named as a tensor is a DEVICE pointer that the
+ *     caller allocated and owns (typically a PyTorch CUDA/HIP tensor).  The
+ *     library allocates no device memory and keeps no state besides the
+ *     loaded code objects; it is re-entrant and may be called concurrently
+ *     on different streams.
+ *   - Every call is asynchronous on `stream` (NULL = the default stream).
+ *     Argument checks run on the host before any launch; a non-LT_OK return
+ *     means nothing was launched, except LT_ERR_HIP (a launch failed).
+ *   - Inputs must not alias outputs (the GEMM's C is both).
+ *   - Float16 outputs are rounded once, round-to-nearest-even, from the
+ *     FP32 accumulator; FP16 subnormals are kept.
+ *   - Fast-path alignment: every half pointer must be 16-byte aligned and
+ *     every leading dimension / row stride a multiple of 8 elements; the
+ *     GEMM also needs M, N, K to be multiples of 8.  Otherwise the call
+ *     returns LT_ERR_UNSUPPORTED (it never computes a wrong result).
+ */
+#ifndef LT_H_
+#define LT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef uint16_t lt_half;
+typedef struct ihipStream_t* lt_stream;
+
+typedef enum {
+  LT_OK = 0,
+  LT_ERR_INVALID_ARG = 1,  /* NULL pointer, negative size, ld too small, ... */
+  LT_ERR_UNSUPPORTED = 2,  /* valid arguments outside what the kernels handle */
+  LT_ERR_WORKSPACE = 3,    /* workspace missing or smaller than required */
+  LT_ERR_HIP = 4           /* a HIP launch or runtime call failed */
+} lt_status;
+
+/* Static description of a status code (never NULL). */
+const char* lt_status_string(lt_status s);
+
+/* Human-readable detail of the last non-LT_OK return on the calling host
+ * thread ("" if none).  The pointer stays valid until the next lt_* call on
+ * this thread. */
+const char* lt_last_error(void);
+
+/* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
+int lt_version(void);
+
+/*
+ * GEMM update (Sec. 4.1, FP16 GEMM backend; the output tile is loaded as the
+ * accumulation buffer):
+ *
+ *     C[M,N] = alpha * op(A)[M,K] * op(B)[K,N] + beta * C[M,N]
+ *
+ *   op(X) = X for trans == 0, X^T for trans == 1.
+ *   A is stored [M, K] (transA = 0, lda >= K) or [K, M] (transA = 1, lda >= M).
+ *   B is stored [K, N] (transB = 0, ldb >= N) or [N, K] (transB = 1, ldb >= K).
+ *   C is stored [M, N], ldc >= N.
+ *   FP32 accumulation, one RNE rounding to FP16 per output element.
+ *   beta == 0 never reads C (NaN / uninitialised C is fine).
+ *   M == 0 or N == 0: no-op.  K == 0: C = beta * C.
+ *   Layer usage with nn.Linear weights W[out, in]:
+ *     forward  Y  = X  W^T  -> (transA, transB) = (0, 1)
+ *     dgrad    dX = dY W    -> (0, 0)
+ *     wgrad    dW = dY^T X  -> (1, 0)   (beta = 1 accumulates micro-batches)
+ *   Errors: LT_ERR_INVALID_ARG for NULL A/B/C (C may be NULL only if M or N
+ *   is 0), negative sizes, trans not 0/1, ld smaller than the row length;
+ *   LT_ERR_UNSUPPORTED for M, N, K or an ld not a multiple of 8 or a pointer
+ *   not 16-byte aligned.
+ */
+lt_status lt_gemm_f16(int transA, int transB, int64_t M, int64_t N, int64_t K,
+                      float alpha, const lt_half* A, int64_t lda,
+                      const lt_half* B, int64_t ldb, float beta, lt_half* C,
+                      int64_t ldc, lt_stream stream);
+
+/*
+ * GEMM with a separate accumulation input (Sec. 4.1's accumulation buffer
+ * read from one place and written to another, e.g. a residual add):
+ *
+ *     C[M,N] = alpha * op(A) op(B) + beta * R[M,N]
+ *
+ *   Same conventions and errors as lt_gemm_f16; R is stored [M, N] with
+ *   ldr >= N and is read only when beta != 0 (then R must not be NULL).
+ *   R may be the same buffer as C (with ldr == ldc; this is lt_gemm_f16) but
+ *   must not partially overlap it.  Layer usage: H1 = X + O Wo^T with
+ *   R = X, C = H1.
+ */
+lt_status lt_gemm_f16_res(int transA, int transB, int64_t M, int64_t N,
+                          int64_t K, float alpha, const lt_half* A,
+                          int64_t lda, const lt_half* B, int64_t ldb,
+                          float beta, const lt_half* R, int64_t ldr,
+                          lt_half* C, int64_t ldc, lt_stream stream);
+
+/*
+ * Attention forward (the forward whose probabilities Algorithm 1 consumes;
+ * Sec. 4.1).  Per batch b and query head h, with key/value head
+ * kv = h / (Hq / Hkv) (contiguous GQA grouping):
+ *
+ *     s_ij   = scale * q_i . k_j           (j <= i when causal)
+ *     P      = row softmax of s
+ *     O_i    = sum_j P_ij v_j
+ *     LSE_i  = ln sum_j exp(s_ij)          (natural log, FP32)
+ *
+ *   Element (b, i, h, c) of Q is Q[(b*S + i) * q_row_stride + h*D + c];
+ *   K and V likewise with kv_row_stride and kv heads; O with o_row_stride.
+ *   So Q, K, V may be column slices of one fused QKV projection output
+ *   [B*S, (Hq + 2 Hkv) D] (K = QKV + Hq*D, V = QKV + (Hq+Hkv)*D).
+ *   LSE is a dense FP32 array [B, Hq, S].  Queries and keys have the same
+ *   length S; causal masking is top-left aligned (query i sees keys 0..i).
+ *   Errors: INVALID_ARG for NULL pointers, B/S/Hq/Hkv < 1, Hq % Hkv != 0,
+ *   causal not 0/1, scale not finite and > 0, strides smaller than the row
+ *   length;
+ *   UNSUPPORTED for D not in {64, 128}, misaligned pointers or strides.
+ */
+lt_status lt_attn_fwd(const lt_half* Q, const lt_half* K, const lt_half* V,
+                      int64_t q_row_stride, int64_t kv_row_stride, lt_half* O,
+                      int64_t o_row_stride, float* LSE, int B, int S, int Hq,
+                      int Hkv, int D, float scale, int causal,
+                      lt_stream stream);
+
+/*
+ * Bytes of device workspace lt_attn_bwd needs: the per-row term
+ * D_i = rowsum(dO_i * O_i) [B, Hq, S] FP32 and the FP32 dQ accumulator
+ * [B, S, Hq, D], each 256-byte aligned.  0 for invalid sizes.
+ */
+size_t lt_attn_bwd_workspace_size(int B, int S, int Hq, int Hkv, int D);
+
+/*
+ * Attention backward (Sec. 4.1, Algorithm 1: GP = GO V^T,
+ * GS = SoftmaxBackward(P, GP), GV = P^T GO, GQ = GS K, GK = GS^T Q).
+ * P is recomputed as exp(scale * q.k - LSE) from the forward's LSE instead of
+ * being read back; SoftmaxBackward is GS_ij = P_ij (GP_ij - D_i) with
+ * D_i = rowsum(dO_i * O_i).  dQ and dK carry the factor `scale`.
+ * dK and dV of a key/value head sum over its Hq/Hkv query heads.
+ *
+ *   Q, K, V, O, dO, LSE: as written by / passed to lt_attn_fwd (O and dO share
+ *   o_row_stride).  dQ uses dq_row_stride, dK and dV use dkv_row_stride, so
+ *   they may be column slices of one fused dQKV buffer.  dQ, dK, dV are
+ *   overwritten.  `workspace` is a device buffer of at least
+ *   lt_attn_bwd_workspace_size(...) bytes, 256-byte aligned, owned by the
+ *   caller; its contents on entry are ignored.
+ *   Errors: as lt_attn_fwd, plus LT_ERR_WORKSPACE if workspace is NULL or
+ *   ws_bytes is too small.
+ */
+lt_status lt_attn_bwd(const lt_half* Q, const lt_half* K, const lt_half* V,
+                      int64_t q_row_stride, int64_t kv_row_stride,
+                      const lt_half* O, const lt_half* dO,
+                      int64_t o_row_stride, const float* LSE, lt_half* dQ,
+                      lt_half* dK, lt_half* dV, int64_t dq_row_stride,
+                      int64_t dkv_row_stride, void* workspace, size_t ws_bytes,
+                      int B, int S, int Hq, int Hkv, int D, float scale,
+                      int causal, lt_stream stream);
+
+/*
+ * SwiGLU gate joining the FFN gate/up projection and the down projection.
+ *   GU is [T, 2F] (row stride 2F): columns 0..F-1 gate G, F..2F-1 up U.
+ *   forward : A[T, F]   = silu(G) * U,  silu(x) = x / (1 + exp(-x))
+ *   backward: dGU[T,2F] = [dA * U * s * (1 + G (1 - s)) | dA * silu(G)],
+ *             s = sigmoid(G)
+ *   Math in FP32, one RNE rounding of each output.
+ *   T == 0 or F == 0: no-op.  Errors: INVALID_ARG for NULL pointers or
+ *   negative sizes; UNSUPPORTED for F not a multiple of 8 or misaligned
+ *   pointers.
+ */
+lt_status lt_swiglu_fwd(const lt_half* GU, lt_half* A, int64_t T, int64_t F,
+                        lt_stream stream);
+lt_status lt_swiglu_bwd(const lt_half* dA, const lt_half* GU, lt_half* dGU,
+                        int64_t T, int64_t F, lt_stream stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LT_H_ */

@@ -1,0 +1,72 @@
+// Shared device helpers of the gfx950 kernels (MFMA wrappers, vector types,
+// LDS swizzles, 8x8 half transposes).  Internal to liblt; not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lt {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half4 __attribute__((ext_vector_type(4)));
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+
+// D[32x32] += A[32x16] * B[16x32], fp16 in, fp32 accumulate.
+// Operand lane layout: lane l supplies row/column (l % 32) and 8 consecutive
+// reduction indices selected by (l / 32); A and B use the same reduction
+// index mapping, so any consistent permutation of the reduction axis is
+// allowed.  Result: lane l holds column (l % 32), rows
+// 8*(r/4) + 4*(l/32) + (r%4) for r = 0..15.
+__device__ __forceinline__ f32x16 mfma32(half8 a, half8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ half8 as_half8(u32x4 v) {
+  return __builtin_bit_cast(half8, v);
+}
+__device__ __forceinline__ u32x4 as_u32x4(half8 v) {
+  return __builtin_bit_cast(u32x4, v);
+}
+
+// 16-byte global load / store helpers.
+__device__ __forceinline__ u32x4 ld16(const void* p) {
+  return *reinterpret_cast<const u32x4*>(p);
+}
+__device__ __forceinline__ void st16(void* p, u32x4 v) {
+  *reinterpret_cast<u32x4*>(p) = v;
+}
+
+// Transpose an 8x8 block of halves held as 8 rows of 16 bytes:
+// in[r] holds elements (r, 0..7); out[c] receives elements (0..7, c).
+__device__ __forceinline__ void transpose8x8(const u32x4 in[8], u32x4 out[8]) {
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    const int w = c >> 1;
+    const bool hi = c & 1;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t a = in[2 * q][w];
+      const uint32_t b = in[2 * q + 1][w];
+      out[c][q] = hi ? ((a >> 16) | (b & 0xffff0000u)) : ((a & 0xffffu) | (b << 16));
+    }
+  }
+}
+
+// Pack 8 fp32 values into 8 fp16 (round to nearest even).
+__device__ __forceinline__ half8 pack8(float a0, float a1, float a2, float a3,
+                                       float a4, float a5, float a6, float a7) {
+  half8 h;
+  h[0] = (_Float16)a0; h[1] = (_Float16)a1; h[2] = (_Float16)a2; h[3] = (_Float16)a3;
+  h[4] = (_Float16)a4; h[5] = (_Float16)a5; h[6] = (_Float16)a6; h[7] = (_Float16)a7;
+  return h;
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+}  // namespace lt

@@ -1,0 +1,78 @@
+// Internal launcher interface between the C ABI layer (lt_api.cpp) and the
+// kernel translation units.  Arguments are validated before these are called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/lt.h"
+
+namespace lt {
+
+struct GemmArgs {
+  int transA, transB;
+  int64_t M, N, K;
+  float alpha, beta;
+  const lt_half* A;
+  int64_t lda;
+  const lt_half* B;
+  int64_t ldb;
+  const lt_half* R;   // residual / accumulation input (may equal C)
+  int64_t ldr;
+  lt_half* C;
+  int64_t ldc;
+};
+
+struct AttnShape {
+  int B, S, Hq, Hkv, D;
+  float scale;
+  int causal;
+};
+
+struct AttnFwdArgs {
+  AttnShape sh;
+  const lt_half* Q;
+  const lt_half* K;
+  const lt_half* V;
+  int64_t q_stride, kv_stride;
+  lt_half* O;
+  int64_t o_stride;
+  float* LSE;
+};
+
+struct AttnBwdArgs {
+  AttnShape sh;
+  const lt_half* Q;
+  const lt_half* K;
+  const lt_half* V;
+  int64_t q_stride, kv_stride;
+  const lt_half* O;
+  const lt_half* dO;
+  int64_t o_stride;
+  const float* LSE;
+  lt_half* dQ;
+  lt_half* dK;
+  lt_half* dV;
+  int64_t dq_stride, dkv_stride;
+  float* delta;   // workspace: [B, Hq, S]
+  float* dq_acc;  // workspace: [B, S, Hq, D]
+};
+
+// Workspace layout of the attention backward (offsets in bytes).
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+inline size_t attn_bwd_delta_bytes(int B, int S, int Hq) {
+  return align256((size_t)B * Hq * S * sizeof(float));
+}
+inline size_t attn_bwd_dq_bytes(int B, int S, int Hq, int D) {
+  return align256((size_t)B * S * Hq * D * sizeof(float));
+}
+
+hipError_t gemm_f16_launch(const GemmArgs& a, hipStream_t s);
+hipError_t attn_fwd_launch(const AttnFwdArgs& a, hipStream_t s);
+hipError_t attn_bwd_launch(const AttnBwdArgs& a, hipStream_t s);
+hipError_t swiglu_fwd_launch(const lt_half* GU, lt_half* A, int64_t T, int64_t F, hipStream_t s);
+hipError_t swiglu_bwd_launch(const lt_half* dA, const lt_half* GU, lt_half* dGU, int64_t T,
+                             int64_t F, hipStream_t s);
+
+}  // namespace lt

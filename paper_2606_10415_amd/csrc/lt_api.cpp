@@ -1,0 +1,196 @@
+// C ABI of liblt: host-side argument validation and dispatch to the gfx950
+// kernels.  Declarations and the full contract are in include/lt.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "kernels.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+lt_status fail(lt_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+lt_status ok() {
+  g_last_error.clear();
+  return LT_OK;
+}
+
+lt_status from_hip(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(LT_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+lt_status check_attn_common(const void* Q, const void* K, const void* V, int64_t q_stride,
+                            int64_t kv_stride, int B, int S, int Hq, int Hkv, int D, float scale,
+                            int causal) {
+  if (!Q || !K || !V) return fail(LT_ERR_INVALID_ARG, "NULL Q/K/V pointer");
+  if (B < 1 || S < 1 || Hq < 1 || Hkv < 1 || D < 1)
+    return fail(LT_ERR_INVALID_ARG, "B, S, Hq, Hkv, D must be >= 1 (got %d %d %d %d %d)", B, S, Hq,
+                Hkv, D);
+  if (Hq % Hkv != 0) return fail(LT_ERR_INVALID_ARG, "Hq (%d) must be a multiple of Hkv (%d)", Hq, Hkv);
+  if (causal != 0 && causal != 1) return fail(LT_ERR_INVALID_ARG, "causal must be 0 or 1");
+  if (!(scale > 0.f) || !std::isfinite(scale))
+    return fail(LT_ERR_INVALID_ARG, "scale must be finite and > 0");
+  if (q_stride < (int64_t)Hq * D)
+    return fail(LT_ERR_INVALID_ARG, "q_row_stride %lld < Hq*D", (long long)q_stride);
+  if (kv_stride < (int64_t)Hkv * D)
+    return fail(LT_ERR_INVALID_ARG, "kv_row_stride %lld < Hkv*D", (long long)kv_stride);
+  if (D != 64 && D != 128) return fail(LT_ERR_UNSUPPORTED, "head dim %d not in {64, 128}", D);
+  if ((q_stride & 7) || (kv_stride & 7))
+    return fail(LT_ERR_UNSUPPORTED, "row strides must be multiples of 8 elements");
+  if (!aligned16(Q) || !aligned16(K) || !aligned16(V))
+    return fail(LT_ERR_UNSUPPORTED, "Q/K/V must be 16-byte aligned");
+  if ((int64_t)B * S * Hq > (int64_t)1 << 31)
+    return fail(LT_ERR_UNSUPPORTED, "B*S*Hq too large");
+  return LT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* lt_status_string(lt_status s) {
+  switch (s) {
+    case LT_OK: return "LT_OK";
+    case LT_ERR_INVALID_ARG: return "LT_ERR_INVALID_ARG";
+    case LT_ERR_UNSUPPORTED: return "LT_ERR_UNSUPPORTED";
+    case LT_ERR_WORKSPACE: return "LT_ERR_WORKSPACE";
+    case LT_ERR_HIP: return "LT_ERR_HIP";
+  }
+  return "LT_ERR_UNKNOWN";
+}
+
+const char* lt_last_error(void) { return g_last_error.c_str(); }
+
+int lt_version(void) { return 100; }
+
+lt_status lt_gemm_f16_res(int transA, int transB, int64_t M, int64_t N, int64_t K, float alpha,
+                          const lt_half* A, int64_t lda, const lt_half* B, int64_t ldb, float beta,
+                          const lt_half* R, int64_t ldr, lt_half* C, int64_t ldc,
+                          lt_stream stream) {
+  if ((transA != 0 && transA != 1) || (transB != 0 && transB != 1))
+    return fail(LT_ERR_INVALID_ARG, "transA/transB must be 0 or 1");
+  if (M < 0 || N < 0 || K < 0) return fail(LT_ERR_INVALID_ARG, "negative GEMM size");
+  if (M == 0 || N == 0) return ok();
+  if (!C) return fail(LT_ERR_INVALID_ARG, "NULL C");
+  if (K > 0 && (!A || !B)) return fail(LT_ERR_INVALID_ARG, "NULL A or B");
+  if (beta != 0.f && !R) return fail(LT_ERR_INVALID_ARG, "beta != 0 needs R");
+  const int64_t a_row = transA ? M : K;
+  const int64_t b_row = transB ? K : N;
+  if (K > 0 && (lda < a_row || ldb < b_row))
+    return fail(LT_ERR_INVALID_ARG, "lda/ldb smaller than the stored row length");
+  if (ldc < N) return fail(LT_ERR_INVALID_ARG, "ldc %lld < N %lld", (long long)ldc, (long long)N);
+  if (beta != 0.f && ldr < N) return fail(LT_ERR_INVALID_ARG, "ldr %lld < N %lld", (long long)ldr, (long long)N);
+  if ((M | N | K) & 7) return fail(LT_ERR_UNSUPPORTED, "M, N, K must be multiples of 8");
+  if (((K > 0 ? (lda | ldb) : 0) | ldc | (beta != 0.f ? ldr : 0)) & 7)
+    return fail(LT_ERR_UNSUPPORTED, "leading dimensions must be multiples of 8");
+  if ((K > 0 && (!aligned16(A) || !aligned16(B))) || !aligned16(C) ||
+      (beta != 0.f && !aligned16(R)))
+    return fail(LT_ERR_UNSUPPORTED, "A, B, R, C must be 16-byte aligned");
+  if (M > (int64_t)1 << 30 || N > (int64_t)1 << 30)
+    return fail(LT_ERR_UNSUPPORTED, "M or N too large for the tile grid");
+  lt::GemmArgs g{transA, transB, M, N, K, alpha, beta, A, lda, B, ldb,
+                 beta != 0.f ? R : C, beta != 0.f ? ldr : ldc, C, ldc};
+  return from_hip(lt::gemm_f16_launch(g, reinterpret_cast<hipStream_t>(stream)), "gemm launch");
+}
+
+lt_status lt_gemm_f16(int transA, int transB, int64_t M, int64_t N, int64_t K, float alpha,
+                      const lt_half* A, int64_t lda, const lt_half* B, int64_t ldb, float beta,
+                      lt_half* C, int64_t ldc, lt_stream stream) {
+  return lt_gemm_f16_res(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, C, ldc, C, ldc,
+                         stream);
+}
+
+lt_status lt_attn_fwd(const lt_half* Q, const lt_half* K, const lt_half* V, int64_t q_row_stride,
+                      int64_t kv_row_stride, lt_half* O, int64_t o_row_stride, float* LSE, int B,
+                      int S, int Hq, int Hkv, int D, float scale, int causal, lt_stream stream) {
+  lt_status st = check_attn_common(Q, K, V, q_row_stride, kv_row_stride, B, S, Hq, Hkv, D, scale,
+                                   causal);
+  if (st != LT_OK) return st;
+  if (!O || !LSE) return fail(LT_ERR_INVALID_ARG, "NULL O or LSE");
+  if (o_row_stride < (int64_t)Hq * D) return fail(LT_ERR_INVALID_ARG, "o_row_stride < Hq*D");
+  if ((o_row_stride & 7) || !aligned16(O))
+    return fail(LT_ERR_UNSUPPORTED, "O must be 16-byte aligned with stride % 8 == 0");
+  if (reinterpret_cast<uintptr_t>(LSE) & 3u) return fail(LT_ERR_UNSUPPORTED, "LSE must be 4-byte aligned");
+  lt::AttnFwdArgs a{{B, S, Hq, Hkv, D, scale, causal}, Q, K, V, q_row_stride, kv_row_stride, O,
+                    o_row_stride, LSE};
+  return from_hip(lt::attn_fwd_launch(a, reinterpret_cast<hipStream_t>(stream)), "attn_fwd launch");
+}
+
+size_t lt_attn_bwd_workspace_size(int B, int S, int Hq, int Hkv, int D) {
+  if (B < 1 || S < 1 || Hq < 1 || Hkv < 1 || D < 1 || Hq % Hkv) return 0;
+  return lt::attn_bwd_delta_bytes(B, S, Hq) + lt::attn_bwd_dq_bytes(B, S, Hq, D);
+}
+
+lt_status lt_attn_bwd(const lt_half* Q, const lt_half* K, const lt_half* V, int64_t q_row_stride,
+                      int64_t kv_row_stride, const lt_half* O, const lt_half* dO,
+                      int64_t o_row_stride, const float* LSE, lt_half* dQ, lt_half* dK, lt_half* dV,
+                      int64_t dq_row_stride, int64_t dkv_row_stride, void* workspace,
+                      size_t ws_bytes, int B, int S, int Hq, int Hkv, int D, float scale,
+                      int causal, lt_stream stream) {
+  lt_status st = check_attn_common(Q, K, V, q_row_stride, kv_row_stride, B, S, Hq, Hkv, D, scale,
+                                   causal);
+  if (st != LT_OK) return st;
+  if (!O || !dO || !LSE || !dQ || !dK || !dV)
+    return fail(LT_ERR_INVALID_ARG, "NULL O/dO/LSE/dQ/dK/dV pointer");
+  if (o_row_stride < (int64_t)Hq * D || dq_row_stride < (int64_t)Hq * D ||
+      dkv_row_stride < (int64_t)Hkv * D)
+    return fail(LT_ERR_INVALID_ARG, "o/dq/dkv row stride smaller than the row length");
+  if ((o_row_stride | dq_row_stride | dkv_row_stride) & 7)
+    return fail(LT_ERR_UNSUPPORTED, "row strides must be multiples of 8 elements");
+  if (!aligned16(O) || !aligned16(dO) || !aligned16(dQ) || !aligned16(dK) || !aligned16(dV))
+    return fail(LT_ERR_UNSUPPORTED, "O/dO/dQ/dK/dV must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(LSE) & 3u) return fail(LT_ERR_UNSUPPORTED, "LSE must be 4-byte aligned");
+  const size_t need = lt_attn_bwd_workspace_size(B, S, Hq, Hkv, D);
+  if (!workspace || ws_bytes < need)
+    return fail(LT_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                workspace ? ws_bytes : (size_t)0);
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  char* ws = static_cast<char*>(workspace);
+  lt::AttnBwdArgs a{{B, S, Hq, Hkv, D, scale, causal},
+                    Q, K, V, q_row_stride, kv_row_stride, O, dO, o_row_stride, LSE, dQ, dK, dV,
+                    dq_row_stride, dkv_row_stride,
+                    reinterpret_cast<float*>(ws),
+                    reinterpret_cast<float*>(ws + lt::attn_bwd_delta_bytes(B, S, Hq))};
+  return from_hip(lt::attn_bwd_launch(a, reinterpret_cast<hipStream_t>(stream)), "attn_bwd launch");
+}
+
+lt_status lt_swiglu_fwd(const lt_half* GU, lt_half* A, int64_t T, int64_t F, lt_stream stream) {
+  if (T < 0 || F < 0) return fail(LT_ERR_INVALID_ARG, "negative size");
+  if (T == 0 || F == 0) return ok();
+  if (!GU || !A) return fail(LT_ERR_INVALID_ARG, "NULL pointer");
+  if (F & 7) return fail(LT_ERR_UNSUPPORTED, "F must be a multiple of 8");
+  if (!aligned16(GU) || !aligned16(A)) return fail(LT_ERR_UNSUPPORTED, "pointers must be 16-byte aligned");
+  return from_hip(lt::swiglu_fwd_launch(GU, A, T, F, reinterpret_cast<hipStream_t>(stream)),
+                  "swiglu_fwd launch");
+}
+
+lt_status lt_swiglu_bwd(const lt_half* dA, const lt_half* GU, lt_half* dGU, int64_t T, int64_t F,
+                        lt_stream stream) {
+  if (T < 0 || F < 0) return fail(LT_ERR_INVALID_ARG, "negative size");
+  if (T == 0 || F == 0) return ok();
+  if (!dA || !GU || !dGU) return fail(LT_ERR_INVALID_ARG, "NULL pointer");
+  if (F & 7) return fail(LT_ERR_UNSUPPORTED, "F must be a multiple of 8");
+  if (!aligned16(dA) || !aligned16(GU) || !aligned16(dGU))
+    return fail(LT_ERR_UNSUPPORTED, "pointers must be 16-byte aligned");
+  return from_hip(lt::swiglu_bwd_launch(dA, GU, dGU, T, F, reinterpret_cast<hipStream_t>(stream)),
+                  "swiglu_bwd launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,129 @@
+"""CPU checks of the C ABI: the library loads, exports every function that
+include/lt.h declares, and rejects bad arguments on the host before any GPU
+work (these paths make no HIP call, so they run without a GPU)."""
+
+import ctypes
+
+import pytest
+
+from paper_2606_10415_amd import lt
+
+
+def test_every_declared_symbol_is_exported():
+    names = lt.declared_functions()
+    assert {"lt_gemm_f16", "lt_gemm_f16_res", "lt_attn_fwd", "lt_attn_bwd",
+            "lt_attn_bwd_workspace_size", "lt_swiglu_fwd", "lt_swiglu_bwd",
+            "lt_status_string", "lt_last_error", "lt_version"} <= set(names)
+    for n in names:
+        assert hasattr(lt._lib, n), f"{n} declared in lt.h but not exported"
+
+
+def test_status_strings():
+    assert lt.status_string(lt.LT_OK) == "LT_OK"
+    assert lt.status_string(lt.LT_ERR_INVALID_ARG) == "LT_ERR_INVALID_ARG"
+    assert lt.status_string(lt.LT_ERR_UNSUPPORTED) == "LT_ERR_UNSUPPORTED"
+    assert lt.status_string(lt.LT_ERR_WORKSPACE) == "LT_ERR_WORKSPACE"
+    assert lt.status_string(lt.LT_ERR_HIP) == "LT_ERR_HIP"
+    assert lt.status_string(99) == "LT_ERR_UNKNOWN"
+    assert lt.lt_version() >= 100
+
+
+FAKE = 0x1000_0000   # 16-byte aligned address that is never dereferenced (host-side rejection)
+
+
+def _gemm(**kw):
+    a = dict(transA=0, transB=1, M=64, N=64, K=64, alpha=1.0, A=FAKE, lda=64, B=FAKE, ldb=64,
+             beta=0.0, C=FAKE, ldc=64)
+    a.update(kw)
+    return lt._lib.lt_gemm_f16(a["transA"], a["transB"], a["M"], a["N"], a["K"], a["alpha"], a["A"],
+                               a["lda"], a["B"], a["ldb"], a["beta"], a["C"], a["ldc"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(transA=2), lt.LT_ERR_INVALID_ARG),
+    (dict(M=-1), lt.LT_ERR_INVALID_ARG),
+    (dict(A=None), lt.LT_ERR_INVALID_ARG),
+    (dict(C=None), lt.LT_ERR_INVALID_ARG),
+    (dict(lda=32), lt.LT_ERR_INVALID_ARG),
+    (dict(ldc=8), lt.LT_ERR_INVALID_ARG),
+    (dict(M=60), lt.LT_ERR_UNSUPPORTED),
+    (dict(K=20, lda=20, ldb=20), lt.LT_ERR_UNSUPPORTED),
+    (dict(lda=68), lt.LT_ERR_UNSUPPORTED),
+    (dict(A=FAKE + 2), lt.LT_ERR_UNSUPPORTED),
+])
+def test_gemm_rejects_on_host(kw, status):
+    assert _gemm(**kw) == status
+    assert lt.last_error() != ""
+
+
+def test_gemm_empty_is_noop():
+    # M == 0 or N == 0: nothing to do, nothing launched, pointers never read
+    assert _gemm(M=0, A=None, B=None, C=None) == lt.LT_OK
+    assert _gemm(N=0, A=None, B=None, C=None) == lt.LT_OK
+
+
+def test_gemm_res_needs_r_when_beta_nonzero():
+    st = lt._lib.lt_gemm_f16_res(0, 1, 64, 64, 64, 1.0, FAKE, 64, FAKE, 64, 1.0, None, 64, FAKE, 64, None)
+    assert st == lt.LT_ERR_INVALID_ARG
+
+
+def _fwd(**kw):
+    a = dict(Q=FAKE, K=FAKE, V=FAKE, qs=384, kvs=384, O=FAKE, os=128, LSE=FAKE, B=1, S=16, Hq=2,
+             Hkv=1, D=64, scale=0.125, causal=1)
+    a.update(kw)
+    return lt._lib.lt_attn_fwd(a["Q"], a["K"], a["V"], a["qs"], a["kvs"], a["O"], a["os"], a["LSE"],
+                               a["B"], a["S"], a["Hq"], a["Hkv"], a["D"], a["scale"], a["causal"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(Q=None), lt.LT_ERR_INVALID_ARG),
+    (dict(LSE=None), lt.LT_ERR_INVALID_ARG),
+    (dict(S=0), lt.LT_ERR_INVALID_ARG),
+    (dict(Hq=3, Hkv=2), lt.LT_ERR_INVALID_ARG),
+    (dict(causal=2), lt.LT_ERR_INVALID_ARG),
+    (dict(scale=0.0), lt.LT_ERR_INVALID_ARG),
+    (dict(scale=float("nan")), lt.LT_ERR_INVALID_ARG),
+    (dict(qs=64), lt.LT_ERR_INVALID_ARG),
+    (dict(os=64), lt.LT_ERR_INVALID_ARG),
+    (dict(D=32, qs=384, os=128), lt.LT_ERR_UNSUPPORTED),
+    (dict(D=96), lt.LT_ERR_UNSUPPORTED),
+    (dict(qs=388), lt.LT_ERR_UNSUPPORTED),
+    (dict(K=FAKE + 8), lt.LT_ERR_UNSUPPORTED),
+])
+def test_attn_fwd_rejects_on_host(kw, status):
+    assert _fwd(**kw) == status
+
+
+def test_attn_bwd_workspace():
+    ws = lt.lt_attn_bwd_workspace_size(2, 100, 8, 2, 128)
+    assert ws >= 4 * 2 * 8 * 100 + 4 * 2 * 100 * 8 * 128
+    assert ws % 256 == 0
+    assert lt.lt_attn_bwd_workspace_size(0, 100, 8, 2, 128) == 0
+    assert lt.lt_attn_bwd_workspace_size(1, 100, 8, 3, 128) == 0
+    args = [FAKE, FAKE, FAKE, 1536, 1536, FAKE, FAKE, 1024, FAKE, FAKE, FAKE, FAKE, 1536, 1536]
+    st = lt._lib.lt_attn_bwd(*args, FAKE, ws - 1, 2, 100, 8, 2, 128, 0.09, 1, None)
+    assert st == lt.LT_ERR_WORKSPACE
+    st = lt._lib.lt_attn_bwd(*args, None, ws, 2, 100, 8, 2, 128, 0.09, 1, None)
+    assert st == lt.LT_ERR_WORKSPACE
+    st = lt._lib.lt_attn_bwd(*args, FAKE + 16, ws, 2, 100, 8, 2, 128, 0.09, 1, None)
+    assert st == lt.LT_ERR_WORKSPACE
+
+
+def test_swiglu_rejects_on_host():
+    assert lt._lib.lt_swiglu_fwd(FAKE, FAKE, 4, 12, None) == lt.LT_ERR_UNSUPPORTED
+    assert lt._lib.lt_swiglu_fwd(None, FAKE, 4, 16, None) == lt.LT_ERR_INVALID_ARG
+    assert lt._lib.lt_swiglu_bwd(FAKE, FAKE, FAKE, -1, 16, None) == lt.LT_ERR_INVALID_ARG
+    assert lt._lib.lt_swiglu_fwd(None, None, 0, 16, None) == lt.LT_OK
+
+
+def test_binding_refuses_host_tensors():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros(8, 8, dtype=torch.float16)
+    with pytest.raises(TypeError):
+        lt.lt_swiglu_fwd(x, x, 8, 4)
+
+
+def test_errors_raise_lt_error():
+    with pytest.raises(lt.LtError) as e:
+        lt.lt_gemm_f16(0, 1, -1, 8, 8, 1.0, FAKE, 8, FAKE, 8, 0.0, FAKE, 8, stream=0)
+    assert e.value.status == lt.LT_ERR_INVALID_ARG

@@ -1,0 +1,136 @@
+"""GPU parity of lt_gemm_f16 / lt_gemm_f16_res against the float64 oracle.
+
+Bars (written here, derived in the design doc):
+  * integer-valued inputs (|partial sums| < 2^24, exact in FP32): the FP16
+    output equals RNE(oracle) bit for bit -- pins layouts, transposes, tails,
+    alpha/beta and the residual operand with zero tolerance;
+  * normal inputs: relative Frobenius error <= 5e-3;
+  * full-size decoder-layer shapes: 1024 sampled entries per GEMM, each an
+    oracle dot product of length K, same 5e-3 bound.
+"""
+
+import itertools
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_10415_amd.synth import normal_f16, uniform_int_f16, WORKLOADS
+from conftest import rel_f
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from paper_2606_10415_amd import lt
+    return torch, lt
+
+
+def _stored(x, trans):
+    return np.ascontiguousarray(x.T) if trans else np.ascontiguousarray(x)
+
+
+def _run(env, transA, transB, M, N, K, alpha, a, b, beta=0.0, c=None, r=None):
+    torch, lt = env
+    A = torch.from_numpy(_stored(a, transA)).cuda()
+    B = torch.from_numpy(_stored(b, transB)).cuda()
+    lda, ldb = A.shape[1], B.shape[1]
+    if c is None:
+        C = torch.full((M, N), float("nan"), dtype=torch.float16, device="cuda")
+    else:
+        C = torch.from_numpy(np.ascontiguousarray(c)).cuda()
+    if r is None:
+        lt.lt_gemm_f16(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, C, N)
+    else:
+        R = torch.from_numpy(np.ascontiguousarray(r)).cuda()
+        lt.lt_gemm_f16_res(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, R, N, C, N)
+    torch.cuda.synchronize()
+    return C.cpu().numpy()
+
+
+LAYOUTS = list(itertools.product([0, 1], [0, 1]))
+
+
+@pytest.mark.parametrize("transA,transB", LAYOUTS)
+@pytest.mark.parametrize("M,N,K", [(8, 8, 8), (136, 200, 72), (264, 520, 1000), (4096, 4096, 512)])
+def test_gemm_exact_integers_bitwise(env, transA, transB, M, N, K):
+    print(f"gemm exact ints trans=({transA},{transB}) M={M} N={N} K={K}", flush=True)
+    a = uniform_int_f16(1, (M, K), -2, 2)
+    b = uniform_int_f16(2, (K, N), -2, 2)
+    c = uniform_int_f16(3, (M, N), -8, 8)
+    got = _run(env, transA, transB, M, N, K, 3.0, a, b, -2.0, c)
+    ref = oracle.gemm(0, 0, 3.0, a, b, -2.0, c).astype(np.float16)
+    assert np.array_equal(got.view(np.uint16), ref.view(np.uint16))
+
+
+@pytest.mark.parametrize("transA,transB", LAYOUTS)
+def test_gemm_residual_operand_bitwise(env, transA, transB):
+    M, N, K = 200, 136, 264
+    a = uniform_int_f16(4, (M, K), -2, 2)
+    b = uniform_int_f16(5, (K, N), -2, 2)
+    r = uniform_int_f16(6, (M, N), -100, 100)
+    got = _run(env, transA, transB, M, N, K, 1.0, a, b, 1.0, None, r)
+    ref = oracle.gemm(0, 0, 1.0, a, b, 1.0, r).astype(np.float16)
+    assert np.array_equal(got.view(np.uint16), ref.view(np.uint16))
+
+
+def test_gemm_beta_zero_ignores_nan_and_k_zero(env):
+    torch, lt = env
+    a = normal_f16(7, (64, 32))
+    b = normal_f16(8, (32, 48))
+    c = np.full((64, 48), np.nan, np.float16)
+    got = _run(env, 0, 0, 64, 48, 32, 1.0, a, b, 0.0, c)
+    assert np.isfinite(got).all()
+    # K == 0: C = beta * C
+    c2 = normal_f16(9, (64, 48))
+    C = torch.from_numpy(c2).cuda()
+    lt.lt_gemm_f16(0, 0, 64, 48, 0, 1.0, None, 0, None, 0, 0.5, C, 48)
+    torch.cuda.synchronize()
+    ref = (0.5 * c2.astype(np.float64)).astype(np.float16)
+    assert np.array_equal(C.cpu().numpy().view(np.uint16), ref.view(np.uint16))
+
+
+@pytest.mark.parametrize("transA,transB", LAYOUTS)
+@pytest.mark.parametrize("M,N,K", [(256, 768, 256), (256, 256, 1376), (1376, 256, 256), (520, 1032, 688)])
+def test_gemm_normal_parity(env, transA, transB, M, N, K):
+    a = normal_f16(10, (M, K))
+    b = normal_f16(11, (K, N), 0.02)
+    c = normal_f16(12, (M, N))
+    got = _run(env, transA, transB, M, N, K, 1.0, a, b, 1.0, c)
+    ref = oracle.gemm(0, 0, 1.0, a, b, 1.0, c)
+    assert rel_f(got, ref) <= 5e-3
+
+
+def _layer_gemms(w):
+    T = w.T
+    return [("qkv_fwd", 0, 1, T, w.qkv_cols, w.H), ("o_fwd", 0, 1, T, w.H, w.Hq * w.D),
+            ("gu_fwd", 0, 1, T, 2 * w.F, w.H), ("down_fwd", 0, 1, T, w.H, w.F),
+            ("down_dgrad", 0, 0, T, w.F, w.H), ("gu_dgrad", 0, 0, T, w.H, 2 * w.F),
+            ("qkv_dgrad", 0, 0, T, w.H, w.qkv_cols),
+            ("down_wgrad", 1, 0, w.H, w.F, T), ("gu_wgrad", 1, 0, 2 * w.F, w.H, T),
+            ("qkv_wgrad", 1, 0, w.qkv_cols, w.H, T)]
+
+
+@pytest.mark.parametrize("name,transA,transB,M,N,K", _layer_gemms(WORKLOADS["llama2-7b"]))
+def test_gemm_full_size_sampled(env, name, transA, transB, M, N, K):
+    """LLaMA-2-7B layer GEMM shapes, the launch configuration the benchmark times."""
+    print(f"gemm full-size {name} M={M} N={N} K={K}", flush=True)
+    torch, lt = env
+    seed = 5000 + 10 * [n for n, *_ in _layer_gemms(WORKLOADS["llama2-7b"])].index(name)
+    # operands as stored: A [M,K] or [K,M]; B [K,N] or [N,K]
+    a_np = normal_f16(seed, (K, M) if transA else (M, K))
+    b_np = normal_f16(seed + 1, (N, K) if transB else (K, N), 0.02)
+    A = torch.from_numpy(a_np).cuda()
+    B = torch.from_numpy(b_np).cuda()
+    C = torch.empty(M, N, dtype=torch.float16, device="cuda")
+    lt.lt_gemm_f16(transA, transB, M, N, K, 1.0, A, A.shape[1], B, B.shape[1], 0.0, C, N)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(0)
+    rows = rng.integers(0, M, 1024)
+    cols = rng.integers(0, N, 1024)
+    ref = oracle.gemm_entries(transA, transB, 1.0, a_np, b_np, 0.0, None, rows, cols)
+    got = C.cpu().numpy()[rows, cols]
+    assert rel_f(got, ref) <= 5e-3

@@ -1,0 +1,83 @@
+"""GPU parity of the SwiGLU kernels and of the chained decoder layer.
+
+Bars: SwiGLU outputs relative Frobenius error <= 5e-3 (per op, same fp16
+inputs); chained layer (one fp16 input set, the GPU keeps fp16
+intermediates, the oracle keeps float64 throughout): Y, dX and the four
+weight gradients <= 5e-3, dQKV <= 1e-2.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_10415_amd.synth import normal_f16, layer_inputs, WORKLOADS, Workload
+from conftest import rel_f
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from paper_2606_10415_amd import lt
+    return torch, lt
+
+
+@pytest.mark.parametrize("T,F", [(256, 688), (1, 8), (37, 104), (4096, 11008)])
+def test_swiglu_parity(env, T, F):
+    print(f"swiglu T={T} F={F}", flush=True)
+    torch, lt = env
+    gu = normal_f16(31, (T, 2 * F), 2.0)
+    da = normal_f16(32, (T, F))
+    GU = torch.from_numpy(gu).cuda()
+    dA = torch.from_numpy(da).cuda()
+    A = torch.empty(T, F, dtype=torch.float16, device="cuda")
+    dGU = torch.empty(T, 2 * F, dtype=torch.float16, device="cuda")
+    lt.lt_swiglu_fwd(GU, A, T, F)
+    lt.lt_swiglu_bwd(dA, GU, dGU, T, F)
+    torch.cuda.synchronize()
+    assert rel_f(A.cpu().numpy(), oracle.swiglu_fwd(gu)) <= 5e-3
+    assert rel_f(dGU.cpu().numpy(), oracle.swiglu_bwd(da, gu)) <= 5e-3
+
+
+def test_swiglu_extreme_inputs(env):
+    torch, lt = env
+    g = np.array([[-1e4, -90.0, -20.0, 0.0, 20.0, 90.0, 1e4, -0.0]], np.float16)
+    gu = np.concatenate([g, np.ones_like(g)], axis=1)
+    GU = torch.from_numpy(gu).cuda()
+    A = torch.empty(1, 8, dtype=torch.float16, device="cuda")
+    dGU = torch.empty(1, 16, dtype=torch.float16, device="cuda")
+    lt.lt_swiglu_fwd(GU, A, 1, 8)
+    lt.lt_swiglu_bwd(torch.ones(1, 8, dtype=torch.float16, device="cuda"), GU, dGU, 1, 8)
+    torch.cuda.synchronize()
+    a = A.cpu().numpy().astype(np.float64)
+    assert np.isfinite(a).all() and np.isfinite(dGU.cpu().numpy()).all()
+    np.testing.assert_allclose(a, oracle.swiglu_fwd(gu), rtol=2e-3, atol=1e-6)
+
+
+def _chained(env, w):
+    torch, lt = env
+    from paper_2606_10415_amd.layer import DecoderLayer
+    p = layer_inputs(w)
+    L = DecoderLayer(w, p)
+    L.step()
+    torch.cuda.synchronize()
+    return p, L
+
+
+@pytest.mark.parametrize("w", [WORKLOADS["tiny"],
+                               Workload("tiny-gqa", 10, B=2, S=136, H=256, Hq=4, Hkv=2, D=64, F=344)],
+                         ids=["tiny", "tiny-gqa-ragged"])
+def test_layer_chained_parity(env, w):
+    print(f"layer chained {w.name}", flush=True)
+    p, L = _chained(env, w)
+    sh = oracle.LayerShape(w.B, w.S, w.H, w.Hq, w.Hkv, w.D, w.F)
+    acts = oracle.layer_fwd(sh, p["X"], p["Wqkv"], p["Wo"], p["Wgu"], p["Wd"])
+    grads = oracle.layer_bwd(sh, p["X"], p["Wqkv"], p["Wo"], p["Wgu"], p["Wd"], p["dY"], acts)
+    c = lambda t: t.cpu().numpy()
+    assert rel_f(c(L.Y), acts["Y"]) <= 5e-3
+    assert rel_f(c(L.dX), grads["dX"]) <= 5e-3
+    for name in ("dWqkv", "dWo", "dWgu", "dWd"):
+        assert rel_f(c(getattr(L, name)), grads[name]) <= 5e-3, name
+    assert rel_f(c(L.dQKV), grads["dQKV"]) <= 1e-2
