@@ -80,8 +80,8 @@ int lt_version(void);
  *     wgrad    dW = dY^T X  -> (1, 0)   (beta = 1 accumulates micro-batches)
  *   Errors: LT_ERR_INVALID_ARG for NULL A/B/C (C may be NULL only if M or N
  *   is 0), negative sizes, trans not 0/1, ld smaller than the row length;
- *   LT_ERR_UNSUPPORTED for M, N, K or an ld not a multiple of 8 or a pointer
- *   not 16-byte aligned.
+ *   LT_ERR_UNSUPPORTED for M, N, K or an ld not a multiple of 8, a pointer
+ *   not 16-byte aligned, or lda / ldb >= 2^22 elements.
  */
 lt_status lt_gemm_f16(int transA, int transB, int64_t M, int64_t N, int64_t K,
                       float alpha, const lt_half* A, int64_t lda,

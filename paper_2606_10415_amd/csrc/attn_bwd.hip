@@ -364,7 +364,9 @@ attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
     __syncthreads();   // dS complete; Q-side tiles no longer read
     if (more) ql.store(smem, tid);
 
-    // ---- dQ^T (partial over this workgroup's keys) = K^T dS^T -> atomics ----
+    // ---- dQ (partial over this workgroup's keys) = dS K -> atomics ----
+    // Result lane layout: column d (one per lane), rows q in 4-runs, so each
+    // atomic instruction covers two 128-byte runs of one dQ row.
 #pragma unroll
     for (int t = 0; t < DQ_BLK; ++t) {
       const int bi = wave * DQ_BLK + t;
@@ -379,15 +381,15 @@ attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
       for (int kc = 0; kc < BKV / 16; ++kc) {
         const half8 ka = as_half8(*reinterpret_cast<const u32x4*>(
             smem + SM::KT_OFF + kr * SM::KT_ROWB + cswz(kr, kc * 2 + g) * 16));
-        const half8 sb = as_half8(*reinterpret_cast<const u32x4*>(
+        const half8 sa = as_half8(*reinterpret_cast<const u32x4*>(
             smem + SM::DS_OFF + qr * SM::DS_ROWB + cswz(qr, kc * 2 + g) * 16));
-        acc = mfma32(ka, sb, acc);
+        acc = mfma32(sa, ka, acc);
       }
-      const int q = qbase + qr;
-      if (q < S) {
-        float* dst = dq_acc + (((int64_t)b * S + q) * Hq + h) * D + db * 32 + 4 * g;
+      float* dst = dq_acc + ((int64_t)b * S * Hq + h) * D + db * 32 + lrow;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) unsafeAtomicAdd(dst + 8 * (r >> 2) + (r & 3), acc[r]);
+      for (int r = 0; r < 16; ++r) {
+        const int q = qbase + qb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+        if (q < S) unsafeAtomicAdd(dst + (int64_t)q * Hq * D, acc[r]);
       }
     }
     __syncthreads();   // next tile's Q-side data visible; dS reads done

@@ -69,4 +69,37 @@ __device__ __forceinline__ half8 pack8(float a0, float a1, float a2, float a3,
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// ---- buffer resources, direct global->LDS loads, LDS transpose reads ----
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef short v4s __attribute__((ext_vector_type(4)));
+#define LT_LDS __attribute__((address_space(3)))
+
+// Raw buffer over `bytes` bytes at p: loads at offsets >= bytes return 0.
+__device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, 0x00020000);
+}
+// Offset that is always out of range: the load returns zeros.
+constexpr uint32_t kOOB = 0x80000000u;
+
+// Direct load of 16 bytes per lane into LDS: lane l's bytes land at
+// lds + 16*l (one contiguous KiB per wave).  lds must be wave-uniform.
+__device__ __forceinline__ void lds_dma16(rsrc_t r, void* lds, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (LT_LDS void*)lds, 16, (int)voff, (int)soff, 0, 0);
+}
+
+// ds_read_b64_tr_b16: within each 16-lane group, lane l receives element
+// (l % 4) of the 8-byte chunks read by lanes (l/4) + 4q, q = 0..3.
+__device__ __forceinline__ v4s lds_read_tr16(const void* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((LT_LDS v4s*)(p));
+}
+
+__device__ __forceinline__ u32x4 pack_v4s_pair(v4s a, v4s b) {
+  u32x4 w;
+  w[0] = (uint32_t)(uint16_t)a[0] | ((uint32_t)(uint16_t)a[1] << 16);
+  w[1] = (uint32_t)(uint16_t)a[2] | ((uint32_t)(uint16_t)a[3] << 16);
+  w[2] = (uint32_t)(uint16_t)b[0] | ((uint32_t)(uint16_t)b[1] << 16);
+  w[3] = (uint32_t)(uint16_t)b[2] | ((uint32_t)(uint16_t)b[3] << 16);
+  return w;
+}
+
 }  // namespace lt

@@ -1,117 +1,138 @@
-// FP16 GEMM update C = alpha * op(A) op(B) + beta * C for gfx950.
+// FP16 GEMM update C = alpha * op(A) op(B) + beta * R for gfx950.
 //
-// Sec. 4.1 of the paper describes the GEMM primitive (C tile loaded as the
-// accumulation buffer) that serves the QKV / output / FFN projections in
+// Sec. 4.1 of the paper describes the GEMM primitive (output tile loaded as
+// the accumulation buffer) that serves the QKV / output / FFN projections in
 // forward, data-gradient and weight-gradient form.  The MT-3000 dataflow
 // (DDR -> GSM -> SM / AM staging, VLIW micro-kernel) is replaced here by the
 // CDNA4 form of the same idea:
-//   * a workgroup owns a BM x BN output tile held in MFMA accumulators;
-//   * K is walked in BK = 64 slices, double-buffered in LDS, with the next
-//     slice's global loads in flight while the current one feeds MFMA
-//     (the overlap of operand preparation with MACs that the paper's
-//     micro-kernel pipeline achieves);
-//   * both operands are kept K-contiguous in LDS whatever their layout in
-//     HBM: an operand whose HBM layout is M- or N-contiguous (dgrad B,
-//     wgrad A and B) is transposed in registers (8x8 half blocks) between
-//     the coalesced 16-byte global load and the LDS store, so one MFMA inner
-//     loop serves every (transA, transB);
-//   * LDS rows are 128 bytes with the 16-byte chunk index XOR-swizzled by the
-//     row, which keeps the 16-byte MFMA operand reads conflict-free;
-//   * output tiles are ordered so that consecutive tiles of one XCD share A
-//     rows (grouped ordering) and each XCD gets a contiguous range of tiles.
+//   * a workgroup owns a BM x BN output tile held in MFMA accumulators
+//     (32x32x16 FP16 MFMA, FP32 accumulate); 256x256 tiles use 8 waves, two
+//     per SIMD, so that one wave's LDS / barrier waits are covered by the
+//     other's MFMAs;
+//   * K is walked in 64-wide slices, double-buffered in LDS.  Operands move
+//     HBM -> LDS with direct buffer loads (16 B per lane, no register
+//     staging), issued one slice ahead so that they overlap the current
+//     slice's MFMA work -- the overlap of operand preparation with MACs that
+//     the paper's micro-kernel pipeline provides;
+//   * each operand keeps its HBM orientation in LDS.  A K-contiguous operand
+//     (forward A and B, dgrad A) is stored row-major; an M/N-contiguous one
+//     (dgrad B, wgrad A and B) is stored k-major and read with the gfx950
+//     LDS transpose read (ds_read_b64_tr_b16), so every (transA, transB)
+//     runs the same MFMA loop at the same speed;
+//   * LDS positions are XOR-swizzled so that both the direct loads and the
+//     MFMA operand reads are free of bank conflicts;
+//   * tiles are ordered so that each XCD gets a contiguous range of tiles,
+//     grouped eight tile-rows at a time for L2 reuse of A and B.
+//   Buffer loads return zeros out of range, which provides the M, N and K
+//   tails without branches.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace lt {
 namespace {
 
-constexpr int BK = 64;            // K slice per LDS stage (halves)
-constexpr int ROWB = BK * 2;      // bytes per LDS row
-constexpr int CHUNKS = BK / 8;    // 16-byte chunks per LDS row
+constexpr int BK = 64;   // K slice (halves)
 
-__device__ __forceinline__ int swz(int row, int chunk) {   // chunk position in LDS row
-  return chunk ^ (row & 7);
-}
+// One operand tile: R rows (M for A, N for B) x BK.
+//   KC  (K-contiguous in HBM): LDS row-major, 128 B per row; 16-byte chunk c
+//       of row r sits at position c ^ (r & 7).
+//   !KC (row index contiguous in HBM): LDS k-major, 2R bytes per k-row;
+//       16-byte chunk c (rows 8c..8c+7) of k-row k sits at position
+//       ((c >> 2) ^ (k & 3)) * 4 + (c & 3).
+template <int R, bool KC, int NT>
+struct Operand {
+  static constexpr int BYTES = R * BK * 2;
+  static constexpr int NINST = BYTES / 1024;        // 1 KiB direct loads per slice
+  static constexpr int PERW = NINST / (NT / 64);     // ... per wave
+  static_assert(NINST % (NT / 64) == 0, "slice must split across waves");
+  static constexpr int KR_PER = 1024 / (2 * R);      // !KC: k-rows per direct load
+  static constexpr int LPR = 64 / KR_PER;            // !KC: lanes per k-row
 
-// Global -> register staging of one operand tile (R rows x BK), "rows" being
-// M for A and N for B.  KCONTIG: the operand is stored with K contiguous
-// (row r of the tile is a K-run at base + r*ld); otherwise it is stored with
-// the row index contiguous (K-run r at base + k*ld + r).
-template <int R, int NT, bool KCONTIG>
-struct TileLoader {
-  // K-contiguous: 16-byte chunks, R*BK/8 per tile.  Row-contiguous: 8x8
-  // blocks (8 k-runs of 8 rows), (R/8)*(BK/8) per tile; threads beyond the
-  // block count idle during staging.
-  static constexpr int TOTAL = KCONTIG ? R * CHUNKS : (R / 8) * (BK / 8);
-  static constexpr int PER = (TOTAL + NT - 1) / NT;
-  static constexpr int NREG = KCONTIG ? PER : PER * 8;
-  static_assert(!KCONTIG || TOTAL % NT == 0, "chunk count must divide evenly");
-  u32x4 reg[NREG];
+  uint32_t voff[PERW];
+  const lt_half* base;
+  int64_t ld, row0;
+  uint32_t nrec;
 
-  __device__ __forceinline__ void load(const lt_half* __restrict__ base, int64_t ld,
-                                       int64_t row0, int64_t rows, int64_t k0, int64_t K,
-                                       int tid) {
-    if constexpr (KCONTIG) {
+  __device__ __forceinline__ void init(const lt_half* b, int64_t ld_, int64_t row0_, int64_t rows,
+                                       int wave, int lane) {
+    base = b;
+    ld = ld_;
+    row0 = row0_;
+    if constexpr (KC) {
+      // rows past the matrix fall outside the buffer and read as zero
+      const int64_t nvalid = rows - row0 < R ? rows - row0 : R;
+      nrec = (uint32_t)(nvalid * ld * 2);
 #pragma unroll
-      for (int i = 0; i < PER; ++i) {
-        const int id = tid + i * NT;
-        const int r = id / CHUNKS;
-        const int c = id % CHUNKS;
-        const int64_t gr = row0 + r;
-        const int64_t gk = k0 + c * 8;
-        if (gr < rows && gk < K)
-          reg[i] = ld16(base + gr * ld + gk);
-        else
-          reg[i] = u32x4{0, 0, 0, 0};
+      for (int t = 0; t < PERW; ++t) {
+        const int r = (wave * PERW + t) * 8 + lane / 8;
+        const int c = (lane % 8) ^ (r & 7);
+        voff[t] = (uint32_t)((r * ld + c * 8) * 2);
       }
     } else {
+      nrec = 0x7fffffff;
 #pragma unroll
-      for (int bi = 0; bi < PER; ++bi) {
-        const int blk = tid + bi * NT;
-        const int rb = blk % (R / 8);
-        const int kb = blk / (R / 8);
-        const int64_t gr = row0 + rb * 8;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int64_t gk = k0 + kb * 8 + j;
-          if (blk < TOTAL && gr < rows && gk < K)
-            reg[bi * 8 + j] = ld16(base + gk * ld + gr);
-          else
-            reg[bi * 8 + j] = u32x4{0, 0, 0, 0};
-        }
+      for (int t = 0; t < PERW; ++t) {
+        const int k = (wave * PERW + t) * KR_PER + lane / LPR;
+        const int p = lane % LPR;
+        const int c = (((p >> 2) ^ (k & 3)) << 2) | (p & 3);
+        voff[t] = row0 + c * 8 < rows ? (uint32_t)((k * ld + c * 8) * 2) : kOOB;
       }
     }
   }
 
-  __device__ __forceinline__ void store(char* lds, int tid) {
-    if constexpr (KCONTIG) {
+  // Direct loads of the slice starting at k0 into the LDS tile at `lds`;
+  // kvalid < BK only for the last slice of a ragged K.
+  __device__ __forceinline__ void load(char* lds, int64_t k0, int kvalid, int wave, int lane) const {
+    if constexpr (KC) {
+      const rsrc_t rs = make_rsrc(base + row0 * ld, nrec);
 #pragma unroll
-      for (int i = 0; i < PER; ++i) {
-        const int id = tid + i * NT;
-        const int r = id / CHUNKS;
-        const int c = id % CHUNKS;
-        *reinterpret_cast<u32x4*>(lds + r * ROWB + swz(r, c) * 16) = reg[i];
+      for (int t = 0; t < PERW; ++t) {
+        const int n = wave * PERW + t;
+        uint32_t off = voff[t];
+        if (kvalid < BK) {
+          const int r = n * 8 + lane / 8;
+          if (((lane % 8) ^ (r & 7)) * 8 >= kvalid) off = kOOB;
+        }
+        lds_dma16(rs, lds + n * 1024, off, (uint32_t)(k0 * 2));
       }
     } else {
+      const rsrc_t rs = make_rsrc(base + k0 * ld + row0, nrec);
 #pragma unroll
-      for (int bi = 0; bi < PER; ++bi) {
-        const int blk = tid + bi * NT;
-        if (blk >= TOTAL) break;
-        const int rb = blk % (R / 8);
-        const int kb = blk / (R / 8);
-        u32x4 t[8];
-        transpose8x8(&reg[bi * 8], t);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int r = rb * 8 + j;
-          *reinterpret_cast<u32x4*>(lds + r * ROWB + swz(r, kb) * 16) = t[j];
-        }
+      for (int t = 0; t < PERW; ++t) {
+        const int n = wave * PERW + t;
+        uint32_t off = voff[t];
+        if (kvalid < BK && n * KR_PER + lane / LPR >= kvalid) off = kOOB;
+        lds_dma16(rs, lds + n * 1024, off, 0);
       }
+    }
+  }
+
+  // MFMA operand: rows rb..rb+31 (lane row = lane % 32), reduction indices
+  // kk*16 + 8*(lane/32) + 0..7.
+  __device__ __forceinline__ half8 frag(const char* lds, int rb, int kk, int lane) const {
+    if constexpr (KC) {
+      const int r = rb + (lane & 31);
+      const int c = kk * 2 + (lane >> 5);
+      return as_half8(*reinterpret_cast<const u32x4*>(lds + r * 128 + ((c ^ (r & 7)) << 4)));
+    } else {
+      // Two transpose reads (h = 0, 1).  Lane L reads 4 rows at
+      // m = rb + 16*((L/16)%2) + 4*(L%4) of k-row kk*16 + 8*(L/32) + 4h + (L%16)/4,
+      // and receives rows rb + L%32 of k-rows kk*16 + 8*(L/32) + 4h + 0..3.
+      const int m = rb + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+      const int c = m >> 3;
+      const int inoff = (m & 7) * 2;
+      v4s part[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int k = kk * 16 + 8 * (lane >> 5) + 4 * h + ((lane & 15) >> 2);
+        const int pc = (((c >> 2) ^ (k & 3)) << 2) | (c & 3);
+        part[h] = lds_read_tr16(lds + k * (2 * R) + pc * 16 + inoff);
+      }
+      return as_half8(pack_v4s_pair(part[0], part[1]));
     }
   }
 };
 
-// BM x BN tile, WGM x WGN waves, each wave (BM/WGM) x (BN/WGN).
 template <int BM, int BN, int WGM, int WGN, bool TA, bool TB>
 __global__ void __launch_bounds__(WGM * WGN * kWave)
 gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
@@ -120,13 +141,12 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
                 const lt_half* R, int64_t ldr, lt_half* C, int64_t ldc, int tiles_m,
                 int tiles_n) {
   constexpr int NT = WGM * WGN * kWave;
-  constexpr int WTM = BM / WGM;      // wave tile rows (M)
-  constexpr int WTN = BN / WGN;      // wave tile cols (N)
-  constexpr int TM = WTM / 32;       // 32x32 MFMA blocks per wave along M
-  constexpr int TN = WTN / 32;
-  constexpr int A_BYTES = BM * ROWB;
-  constexpr int B_BYTES = BN * ROWB;
-  __shared__ __attribute__((aligned(16))) char smem[2 * (A_BYTES + B_BYTES)];
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;   // wave tile
+  constexpr int TM = WTM / 32, TN = WTN / 32;     // 32x32 MFMA blocks per wave
+  using OA = Operand<BM, !TA, NT>;
+  using OB = Operand<BN, TB, NT>;
+  constexpr int STAGE = OA::BYTES + OB::BYTES;
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -143,17 +163,16 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   }
   constexpr int GROUP_M = 8;
   const int group_size = GROUP_M * tiles_n;
-  const int group = pid / group_size;
-  const int first_m = group * GROUP_M;
+  const int first_m = (pid / group_size) * GROUP_M;
   const int gm = min(tiles_m - first_m, GROUP_M);
   const int in_group = pid % group_size;
-  const int tile_m = first_m + in_group % gm;
-  const int tile_n = in_group / gm;
-  const int64_t m0 = (int64_t)tile_m * BM;
-  const int64_t n0 = (int64_t)tile_n * BN;
+  const int64_t m0 = (int64_t)(first_m + in_group % gm) * BM;
+  const int64_t n0 = (int64_t)(in_group / gm) * BN;
 
-  TileLoader<BM, NT, !TA> la;
-  TileLoader<BN, NT, TB> lb;
+  OA oa;
+  OB ob;
+  oa.init(A, lda, m0, M, wave, lane);
+  ob.init(B, ldb, n0, N, wave, lane);
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -164,55 +183,65 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int nk = (int)((K + BK - 1) / BK);
-  if (nk > 0) {
-    la.load(A, lda, m0, M, 0, K, tid);
-    lb.load(B, ldb, n0, N, 0, K, tid);
-    la.store(smem, tid);
-    lb.store(smem + A_BYTES, tid);
-    __syncthreads();
-  }
+  auto kvalid = [&](int kt) {
+    const int64_t rem = K - (int64_t)kt * BK;
+    return rem >= BK ? BK : (int)rem;
+  };
+  half8 fa[2][TM], fb[2][TN];
+  auto frag_load = [&](const char* st, int kk, int s) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) fa[s][i] = oa.frag(st, wm * WTM + i * 32, kk, lane);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) fb[s][j] = ob.frag(st + OA::BYTES, wn * WTN + j * 32, kk, lane);
+  };
 
-  const int lrow = lane & 31;
-  const int lhalf = lane >> 5;
+  if (nk > 0) {
+    oa.load(smem, 0, kvalid(0), wave, lane);
+    ob.load(smem + OA::BYTES, 0, kvalid(0), wave, lane);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
 
   for (int kt = 0; kt < nk; ++kt) {
-    const int stage = kt & 1;
-    char* sa = smem + stage * (A_BYTES + B_BYTES);
-    char* sb = sa + A_BYTES;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      la.load(A, lda, m0, M, (int64_t)(kt + 1) * BK, K, tid);
-      lb.load(B, ldb, n0, N, (int64_t)(kt + 1) * BK, K, tid);
+    char* cur = smem + (kt & 1) * STAGE;
+    char* nxt = smem + ((kt + 1) & 1) * STAGE;
+    // next slice in flight while this one is consumed; its buffer was last
+    // read before the previous barrier
+    if (kt + 1 < nk) {
+      oa.load(nxt, (int64_t)(kt + 1) * BK, kvalid(kt + 1), wave, lane);
+      ob.load(nxt + OA::BYTES, (int64_t)(kt + 1) * BK, kvalid(kt + 1), wave, lane);
     }
+    frag_load(cur, 0, 0);
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      const int chunk = kk * 2 + lhalf;
-      half8 af[TM], bf[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int r = wm * WTM + i * 32 + lrow;
-        af[i] = as_half8(*reinterpret_cast<const u32x4*>(sa + r * ROWB + swz(r, chunk) * 16));
-      }
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int r = wn * WTN + j * 32 + lrow;
-        bf[j] = as_half8(*reinterpret_cast<const u32x4*>(sb + r * ROWB + swz(r, chunk) * 16));
-      }
-      // D[n][m] = sum_k B^T[n][k] A^T[k][m]: lane holds column m, 4-runs of n.
+      const int s = kk & 1;
+      if (kk + 1 < BK / 16) frag_load(cur, kk + 1, s ^ 1);
+      // D[n][m] = sum_k B^T[n][k] A^T[k][m]: lane holds column m, 4-runs of n
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(bf[j], af[i], acc[i][j]);
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(fb[s][j], fa[s][i], acc[i][j]);
+      if (kk + 1 < BK / 16) {
+        // interleave the next step's LDS reads with this step's MFMAs
+        constexpr int NRD = (TA ? 2 : 1) * TM + (TB ? 1 : 2) * TN;
+        constexpr int NMF = TM * TN;
+        constexpr int NPAIR = NRD < NMF ? NRD : NMF;
+#pragma unroll
+        for (int t = 0; t < NPAIR; ++t) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        if (NMF > NPAIR) __builtin_amdgcn_sched_group_barrier(0x008, NMF - NPAIR, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
-    if (more) {
-      char* na = smem + (stage ^ 1) * (A_BYTES + B_BYTES);
-      la.store(na, tid);
-      lb.store(na + A_BYTES, tid);
-    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
 
   // ---- epilogue: C[m][n..n+3] = alpha * acc + beta * R[m][n..n+3] ----
+  const int lrow = lane & 31;
+  const int lhalf = lane >> 5;
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     const int64_t m = m0 + wm * WTM + i * 32 + lrow;
@@ -223,22 +252,18 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
       for (int q = 0; q < 4; ++q) {
         const int64_t n = n0 + wn * WTN + j * 32 + q * 8 + lhalf * 4;
         if (n >= N) continue;
-        lt_half* p = C + m * ldc + n;
-        const lt_half* pr = R + m * ldr + n;
-        float v0 = alpha * acc[i][j][4 * q + 0];
-        float v1 = alpha * acc[i][j][4 * q + 1];
-        float v2 = alpha * acc[i][j][4 * q + 2];
-        float v3 = alpha * acc[i][j][4 * q + 3];
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = alpha * acc[i][j][4 * q + e];
         if (beta != 0.f) {
-          const half4 c = *reinterpret_cast<const half4*>(pr);
-          v0 += beta * (float)c[0];
-          v1 += beta * (float)c[1];
-          v2 += beta * (float)c[2];
-          v3 += beta * (float)c[3];
+          const half4 c = *reinterpret_cast<const half4*>(R + m * ldr + n);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] += beta * (float)c[e];
         }
         half4 o;
-        o[0] = (_Float16)v0; o[1] = (_Float16)v1; o[2] = (_Float16)v2; o[3] = (_Float16)v3;
-        *reinterpret_cast<half4*>(p) = o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = (_Float16)v[e];
+        *reinterpret_cast<half4*>(C + m * ldc + n) = o;
       }
     }
   }
@@ -248,19 +273,18 @@ template <int BM, int BN, int WGM, int WGN, bool TA, bool TB>
 hipError_t launch(const GemmArgs& g, hipStream_t s) {
   const int tiles_m = (int)((g.M + BM - 1) / BM);
   const int tiles_n = (int)((g.N + BN - 1) / BN);
-  const int grid = tiles_m * tiles_n;
-  hipLaunchKernelGGL((gemm_f16_kernel<BM, BN, WGM, WGN, TA, TB>), dim3(grid),
-                     dim3(WGM * WGN * kWave), 0, s, g.M, g.N, g.K, g.alpha, g.A,
-                     g.lda, g.B, g.ldb, g.beta, g.R, g.ldr, g.C, g.ldc, tiles_m, tiles_n);
+  hipLaunchKernelGGL((gemm_f16_kernel<BM, BN, WGM, WGN, TA, TB>), dim3(tiles_m * tiles_n),
+                     dim3(WGM * WGN * kWave), 0, s, g.M, g.N, g.K, g.alpha, g.A, g.lda, g.B, g.ldb,
+                     g.beta, g.R, g.ldr, g.C, g.ldc, tiles_m, tiles_n);
   return hipGetLastError();
 }
 
 template <bool TA, bool TB>
 hipError_t dispatch_tile(const GemmArgs& g, hipStream_t s) {
-  // 256x256 tiles fill the chip once there are >= ~1 tile per CU; smaller
+  // 256x256 tiles once there are about as many tiles as CUs; smaller
   // problems use 128x128 tiles so that more workgroups exist.
   const int64_t big_tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
-  if (big_tiles >= 192) return launch<256, 256, 2, 2, TA, TB>(g, s);
+  if (big_tiles >= 192) return launch<256, 256, 2, 4, TA, TB>(g, s);
   return launch<128, 128, 2, 2, TA, TB>(g, s);
 }
 

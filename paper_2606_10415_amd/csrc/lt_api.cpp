@@ -102,8 +102,10 @@ lt_status lt_gemm_f16_res(int transA, int transB, int64_t M, int64_t N, int64_t 
   if ((K > 0 && (!aligned16(A) || !aligned16(B))) || !aligned16(C) ||
       (beta != 0.f && !aligned16(R)))
     return fail(LT_ERR_UNSUPPORTED, "A, B, R, C must be 16-byte aligned");
-  if (M > (int64_t)1 << 30 || N > (int64_t)1 << 30)
-    return fail(LT_ERR_UNSUPPORTED, "M or N too large for the tile grid");
+  if (M > (int64_t)1 << 30 || N > (int64_t)1 << 30 || K > (int64_t)1 << 30)
+    return fail(LT_ERR_UNSUPPORTED, "M, N or K too large for the tile grid");
+  if (lda >= ((int64_t)1 << 22) || ldb >= ((int64_t)1 << 22))
+    return fail(LT_ERR_UNSUPPORTED, "lda/ldb must be < 2^22 elements (32-bit buffer offsets)");
   lt::GemmArgs g{transA, transB, M, N, K, alpha, beta, A, lda, B, ldb,
                  beta != 0.f ? R : C, beta != 0.f ? ldr : ldc, C, ldc};
   return from_hip(lt::gemm_f16_launch(g, reinterpret_cast<hipStream_t>(stream)), "gemm launch");
