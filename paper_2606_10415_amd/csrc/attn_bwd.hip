@@ -8,24 +8,26 @@
 // SoftmaxBackward is GS = P * (GP - D) with D_i = rowsum(GO_i * O_i).
 //
 // Three kernels:
-//   1. attn_bwd_pre   : D_i = rowsum(dO_i * O_i) (one 8/16-lane group per row,
-//                       lane-group shuffle reduction) and zeroing of the FP32
-//                       dQ accumulator.  HBM-bound.
-//   2. attn_bwd_main  : one workgroup per (batch, kv head, 128-key tile); the
-//                       4 waves own 32 keys each and keep K, V fragments and
-//                       the dK, dV accumulators in registers for the whole
-//                       loop over the GQA group's query heads and the causal
-//                       query tiles (the paper's GSM reduction of GV / GK
-//                       becomes register accumulation inside the workgroup,
-//                       and the GQA sum over query heads is the same loop).
-//                       Q, dO and their transposes are staged through LDS in
-//                       64-query tiles (the next tile's global loads overlap
-//                       the current tile's MFMA work); S = Q K^T and
-//                       dP = dO V^T put one key per lane, so P and dS feed the
-//                       dV / dK MFMAs straight from registers; dS goes through
-//                       LDS once for dQ = dS K, whose FP32 partials are added
-//                       to the workspace with global atomics.
-//   3. attn_bwd_dq    : dQ = scale * accumulator -> FP16.  HBM-bound.
+//   1. attn_bwd_pre : D_i = rowsum(dO_i * O_i) (one 8/16-lane group per row,
+//                     shuffle reduction), LSE in base 2, and zeroing of the
+//                     FP32 dQ accumulator.  HBM-bound.
+//   2. attn_bwd_main: one workgroup per (batch, kv head, 128-key tile); the
+//                     4 waves own 32 keys each and keep K, V fragments and the
+//                     dK, dV accumulators in registers for the whole loop over
+//                     the GQA group's query heads and the causal query tiles
+//                     (the paper's GSM reduction of GV / GK becomes register
+//                     accumulation, and the GQA sum over query heads is the
+//                     same loop).  Q and dO tiles (64 queries) stream HBM ->
+//                     LDS by direct buffer loads, double-buffered one tile
+//                     ahead.  S = Q K^T and dP = dO V^T put one key per lane,
+//                     so P and dS feed the dV / dK MFMAs from registers; the
+//                     Q^T / dO^T operands of those MFMAs are read from the
+//                     same row-layout tiles with the LDS transpose read, in
+//                     the reduction order of the P / dS accumulators.  dS goes
+//                     to LDS once (as dS^T, 8-byte stores) for dQ = dS K, whose
+//                     FP32 partials are added to the workspace with coalesced
+//                     global atomics.
+//   3. attn_bwd_dq  : dQ = scale * accumulator -> FP16.  HBM-bound.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -41,7 +43,8 @@ constexpr float kLog2e = 1.4426950408889634f;
 template <int D>
 __global__ void __launch_bounds__(256)
 attn_bwd_pre_kernel(const lt_half* __restrict__ O, const lt_half* __restrict__ dO, int64_t o_stride,
-                    float* __restrict__ delta, float* __restrict__ dq_acc, int B, int S, int Hq) {
+                    const float* __restrict__ LSE, float* __restrict__ delta,
+                    float* __restrict__ lse2, float* __restrict__ dq_acc, int B, int S, int Hq) {
   constexpr int LPR = D / 8;                       // lanes per row
   const int64_t rows = (int64_t)B * S * Hq;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -67,130 +70,109 @@ attn_bwd_pre_kernel(const lt_half* __restrict__ O, const lt_half* __restrict__ d
     const int64_t bi = row / Hq;
     const int64_t b = bi / S;
     const int64_t i = bi % S;
-    delta[(b * Hq + h) * S + i] = s;
+    const int64_t idx = (b * Hq + h) * S + i;
+    delta[idx] = s;
+    lse2[idx] = LSE[idx] * kLog2e;
   }
 }
 
 // ------------------------------------------------------------ kernel 2
+// Row-layout tile [rows][D] (features contiguous), 2D bytes per row; the
+// 16-byte chunk c of row r sits at chunk c ^ gsw(r).  gsw spreads eight
+// consecutive rows over eight chunk positions (conflict-free row reads) and
+// four consecutive rows over four 64-byte windows (conflict-free transpose
+// reads).
 template <int D>
-struct BwdSmem {
-  static constexpr int ROW_B = D * 2;               // Q / dO row (features contiguous)
-  static constexpr int QT_ROWB = BQ * 2;            // Q^T / dO^T row (64 queries = 128 B)
-  static constexpr int DS_ROWB = BKV * 2;           // dS row (128 keys = 256 B)
-  static constexpr int KT_ROWB = BKV * 2;           // K^T row (128 keys = 256 B)
-  static constexpr int Q_OFF = 0;
-  static constexpr int DO_OFF = Q_OFF + BQ * ROW_B;
-  static constexpr int QT_OFF = DO_OFF + BQ * ROW_B;
-  static constexpr int DOT_OFF = QT_OFF + D * QT_ROWB;
-  static constexpr int LSE_OFF = DOT_OFF + D * QT_ROWB;
-  static constexpr int DEL_OFF = LSE_OFF + BQ * 4;
-  static constexpr int DS_OFF = DEL_OFF + BQ * 4;
-  static constexpr int KT_OFF = DS_OFF + BQ * DS_ROWB;
-  static constexpr int BYTES = KT_OFF + D * KT_ROWB;
+struct RowTile {
+  static constexpr int CPR = D / 8;       // 16-byte chunks per row
+  static constexpr int ROWB = 2 * D;
+  __device__ static __forceinline__ int gsw(int r) { return ((r & 7) ^ ((r & 3) << 2)) & (CPR - 1); }
+  __device__ static __forceinline__ int addr(int r, int c) { return r * ROWB + ((c ^ gsw(r)) << 4); }
+
+  // Direct loads of ROWS rows starting at global row pointer g (row stride
+  // `stride` elements, `valid` rows readable, the rest read as zero), into
+  // the tile at lds, by this wave's share of the 1 KiB blocks.
+  template <int ROWS>
+  __device__ static __forceinline__ void dma(char* lds, const lt_half* g, int64_t stride, int valid,
+                                             int wave, int lane) {
+    constexpr int RPI = 64 / CPR;                 // rows per 1 KiB load
+    constexpr int NINST = ROWS / RPI;
+    static_assert(NINST % NW == 0, "tile must split across waves");
+    const int nv = valid < ROWS ? valid : ROWS;
+    const uint32_t nrec = nv > 0 ? (uint32_t)((int64_t)nv * stride * 2) : 0u;
+#pragma unroll
+    for (int t = 0; t < NINST / NW; ++t) {
+      const int n = wave * (NINST / NW) + t;
+      const int r = n * RPI + lane / CPR;
+      const int c = (lane % CPR) ^ gsw(r);
+      lds_dma16_opaque(g, nrec, lds + n * 1024, (uint32_t)((r * stride + c * 8) * 2));
+    }
+  }
+
+  // A/B operand with rows rb + lane%32 and features kk*16 + 8*(lane/32) + 0..7.
+  __device__ static __forceinline__ half8 row_frag(const char* lds, int rb, int kk, int lane) {
+    return as_half8(*reinterpret_cast<const u32x4*>(lds + addr(rb + (lane & 31), kk * 2 + (lane >> 5))));
+  }
+
+  // Transposed operand (rows of the tile are the reduction index): lane gets
+  // features fb + lane%32 at tile rows
+  //   canonical : kb + 8*(lane/32) + j                    (j = 0..7)
+  //   acc order : kb + 8*(j/4) + 4*(lane/32) + (j%4)       (MFMA accumulator rows)
+  template <bool ACC_ORDER>
+  __device__ static __forceinline__ half8 tr_frag(const char* lds, int kb, int fb, int lane) {
+    const int f = fb + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+    const int c = f >> 3;
+    const int inoff = (f & 7) * 2;
+    v4s part[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int k = ACC_ORDER ? kb + 8 * h + 4 * (lane >> 5) + ((lane & 15) >> 2)
+                              : kb + 8 * (lane >> 5) + 4 * h + ((lane & 15) >> 2);
+      part[h] = lds_read_tr16(lds + addr(k, c) + inoff);
+    }
+    return as_half8(pack_v4s_pair(part[0], part[1]));
+  }
 };
 
-// 16-byte chunk c of a row r at chunk c ^ (r & 7); 8-byte unit u at u ^ (r & 15).
-__device__ __forceinline__ int cswz(int r, int c) { return c ^ (r & 7); }
-__device__ __forceinline__ int uswz(int r, int u) { return u ^ (r & 15); }
-
-// Write 8 consecutive halves (16 bytes, 8-byte units 2k and 2k+1 of a row whose
-// units are swizzled by uswz) into row r of a transposed tile.
-__device__ __forceinline__ void st_units(char* row_base, int r, int k8, u32x4 w) {
-  const int s = r & 15;
-  const int u = (2 * k8) ^ s;
-  if (s & 1) w = u32x4{w[2], w[3], w[0], w[1]};
-  *reinterpret_cast<u32x4*>(row_base + (u & ~1) * 8) = w;
+// dS^T [key][query] tile, 128-byte rows.  Byte offset of (key r, query q):
+// the 64-byte half is XORed with bit 1 of r and the 8-byte slot inside it
+// with bits 2..4 of r, so 32 consecutive keys writing one 8-byte query run
+// hit 32 different bank groups, and the transpose reads of 4 consecutive keys
+// land in 4 different 64-byte windows.
+__device__ __forceinline__ int dst_off(int r, int q) {
+  return r * (BQ * 2) + ((q * 2) ^ (((r >> 1) & 1) << 6) ^ (((r >> 2) & 7) << 3));
 }
 
-// A-operand read from a transposed tile: 8 halves at columns
-// c0 + 4g .. c0 + 4g + 3 and c0 + 8 + 4g .. c0 + 8 + 4g + 3 of row r.
-__device__ __forceinline__ half8 ld_perm8(const char* row_base, int r, int c0, int g) {
-  const int u0 = c0 / 4 + g;
-  const u32x2 lo = *reinterpret_cast<const u32x2*>(row_base + uswz(r, u0) * 8);
-  const u32x2 hi = *reinterpret_cast<const u32x2*>(row_base + uswz(r, u0 + 2) * 8);
-  return as_half8(u32x4{lo[0], lo[1], hi[0], hi[1]});
-}
-
-// Per-thread staging of one query tile: thread t < 128 owns one 8x8 block of
-// Q, thread t >= 128 one of dO (8 queries x 8 features); threads < BQ also
-// fetch LSE (as log2) and D for one query.
 template <int D>
-struct QLoader {
-  static_assert((BQ / 8) * (D / 8) <= 128, "one block per thread");
-  static constexpr int NBLK = (BQ / 8) * (D / 8);
-  u32x4 v[8];
-  float lse2, dl;
-
-  __device__ __forceinline__ void load(const lt_half* __restrict__ Q, const lt_half* __restrict__ dO,
-                                       int64_t q_stride, int64_t o_stride, const float* __restrict__ LSE,
-                                       const float* __restrict__ delta, int b, int h, int S, int Hq,
-                                       int qbase, int tid) {
-    const bool isdo = tid >= 128;
-    const int blk = tid & 127;
-    if (blk < NBLK) {
-      const int db = blk % (D / 8);
-      const int qb = blk / (D / 8);
-      const lt_half* base = isdo ? dO : Q;
-      const int64_t stride = isdo ? o_stride : q_stride;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int q = qbase + qb * 8 + j;
-        v[j] = q < S ? ld16(base + ((int64_t)b * S + q) * stride + (int64_t)h * D + db * 8)
-                     : u32x4{0, 0, 0, 0};
-      }
-    }
-    if (tid < BQ) {
-      const int q = qbase + tid;
-      const int64_t idx = ((int64_t)b * Hq + h) * S + q;
-      lse2 = q < S ? LSE[idx] * kLog2e : INFINITY;
-      dl = q < S ? delta[idx] : 0.f;
-    }
-  }
-
-  __device__ __forceinline__ void store(char* smem, int tid) {
-    using SM = BwdSmem<D>;
-    const bool isdo = tid >= 128;
-    const int blk = tid & 127;
-    if (blk < NBLK) {
-      const int db = blk % (D / 8);
-      const int qb = blk / (D / 8);
-      char* rows = smem + (isdo ? SM::DO_OFF : SM::Q_OFF);
-      char* trows = smem + (isdo ? SM::DOT_OFF : SM::QT_OFF);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int r = qb * 8 + j;
-        *reinterpret_cast<u32x4*>(rows + r * SM::ROW_B + cswz(r, db) * 16) = v[j];
-      }
-      u32x4 t[8];
-      transpose8x8(v, t);     // t[c] = queries qb*8..+7 of feature db*8+c
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const int r = db * 8 + c;
-        st_units(trows + r * SM::QT_ROWB, r, qb, t[c]);
-      }
-    }
-    if (tid < BQ) {
-      reinterpret_cast<float*>(smem + SM::LSE_OFF)[tid] = lse2;
-      reinterpret_cast<float*>(smem + SM::DEL_OFF)[tid] = dl;
-    }
-  }
+struct BwdSmem {
+  using RT = RowTile<D>;
+  static constexpr int TILE_Q = BQ * RT::ROWB;
+  static constexpr int DST_PITCH = BQ * 2;          // dS^T row: 64 queries
+  static constexpr int K_OFF = 0;                     // K tile [BKV][D]
+  static constexpr int Q_OFF = K_OFF + BKV * RT::ROWB;          // 2 buffers
+  static constexpr int DO_OFF = Q_OFF + 2 * TILE_Q;             // 2 buffers
+  static constexpr int LSE_OFF = DO_OFF + 2 * TILE_Q;           // 2 x BQ floats
+  static constexpr int DEL_OFF = LSE_OFF + 2 * BQ * 4;          // 2 x BQ floats
+  static constexpr int DST_OFF = DEL_OFF + 2 * BQ * 4;          // dS^T [BKV][BQ]
+  static constexpr int BYTES = DST_OFF + BKV * DST_PITCH;
 };
 
 template <int D>
 __global__ void __launch_bounds__(NW * 64)
 attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
                      const lt_half* __restrict__ V, int64_t q_stride, int64_t kv_stride,
-                     const lt_half* __restrict__ dO, int64_t o_stride, const float* __restrict__ LSE,
+                     const lt_half* __restrict__ dO, int64_t o_stride, const float* __restrict__ lse2,
                      const float* __restrict__ delta, float* __restrict__ dq_acc,
                      lt_half* __restrict__ dK, lt_half* __restrict__ dV, int64_t dkv_stride, int B,
                      int S, int Hq, int Hkv, float scale, int causal) {
   using SM = BwdSmem<D>;
+  using RT = RowTile<D>;
   constexpr int KK = D / 16;       // MFMA steps over the head dim
   constexpr int DB = D / 32;       // 32-feature blocks
   constexpr int QBS = BQ / 32;     // 32-query blocks per tile
   constexpr int DQ_BLK = DB * QBS / NW;   // dQ output blocks per wave
   static_assert(DQ_BLK >= 1, "dQ blocks must cover the waves");
-  __shared__ __attribute__((aligned(16))) char smem[SM::BYTES];
+  __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -210,6 +192,9 @@ attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
   const lt_half* Kp = K + (int64_t)b * S * kv_stride + (int64_t)kvh * D;
   const lt_half* Vp = V + (int64_t)b * S * kv_stride + (int64_t)kvh * D;
 
+  // ---- K tile -> LDS (B operand of dQ = dS K, read transposed) ----
+  RT::template dma<BKV>(smem + SM::K_OFF, Kp + (int64_t)kbase * kv_stride, kv_stride, S - kbase,
+                        wave, lane);
   // ---- K, V fragments (B operands of S = Q K^T and dP = dO V^T) ----
   half8 kf[KK], vf[KK];
 #pragma unroll
@@ -220,26 +205,6 @@ attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
     } else {
       kf[kk] = as_half8(u32x4{0, 0, 0, 0});
       vf[kk] = as_half8(u32x4{0, 0, 0, 0});
-    }
-  }
-  // ---- K^T tile in LDS (A operand of dQ^T = K^T dS^T) ----
-  {
-    constexpr int NB = (BKV / 8) * (D / 8);
-    for (int blk = tid; blk < NB; blk += NW * 64) {
-      const int db = blk % (D / 8);
-      const int kb = blk / (D / 8);
-      u32x4 v[8], t[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int key = kbase + kb * 8 + j;
-        v[j] = key < S ? ld16(Kp + (int64_t)key * kv_stride + db * 8) : u32x4{0, 0, 0, 0};
-      }
-      transpose8x8(v, t);
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const int r = db * 8 + c;
-        *reinterpret_cast<u32x4*>(smem + SM::KT_OFF + r * SM::KT_ROWB + cswz(r, kb) * 16) = t[c];
-      }
     }
   }
 
@@ -258,54 +223,68 @@ attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
   const int per_head = n_qt - qt0;
   const int n_iter = grp * per_head;
 
-  QLoader<D> ql;
-  if (n_iter > 0) {
-    ql.load(Q, dO, q_stride, o_stride, LSE, delta, b, kvh * grp, S, Hq, qt0 * BQ, tid);
-    ql.store(smem, tid);
-  }
+  // Query tile `it` = (query head, 64 queries).  Q, dO (rows past S read as
+  // zero) and the base-2 LSE and D rows (zero past S: with zero Q and dO rows
+  // those queries contribute nothing) go to LDS by direct loads.
+  auto tile_of = [&](int it, int& h, int& qbase) {
+    h = kvh * grp + it / per_head;
+    qbase = (qt0 + it % per_head) * BQ;
+  };
+  auto stage = [&](int it, int buf) {
+    int h, qbase;
+    tile_of(it, h, qbase);
+    RT::template dma<BQ>(smem + SM::Q_OFF + buf * SM::TILE_Q,
+                         Q + ((int64_t)b * S + qbase) * q_stride + (int64_t)h * D, q_stride,
+                         S - qbase, wave, lane);
+    RT::template dma<BQ>(smem + SM::DO_OFF + buf * SM::TILE_Q,
+                         dO + ((int64_t)b * S + qbase) * o_stride + (int64_t)h * D, o_stride,
+                         S - qbase, wave, lane);
+    if (wave < 2) {
+      const float* rowp = (wave == 0 ? lse2 : delta) + ((int64_t)b * Hq + h) * S + qbase;
+      const int nv = S - qbase < BQ ? S - qbase : BQ;
+      lds_dma4_opaque(rowp, (uint32_t)(nv * 4),
+                      smem + (wave == 0 ? SM::LSE_OFF : SM::DEL_OFF) + buf * BQ * 4,
+                      (uint32_t)(lane * 4));
+    }
+  };
+
+  if (n_iter > 0) stage(0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
-  const float* lse_s = reinterpret_cast<const float*>(smem + SM::LSE_OFF);
-  const float* del_s = reinterpret_cast<const float*>(smem + SM::DEL_OFF);
-
   for (int it = 0; it < n_iter; ++it) {
-    const int h = kvh * grp + it / per_head;
-    const int qbase = (qt0 + it % per_head) * BQ;
+    const int cur = it & 1;
+    int h, qbase;
+    tile_of(it, h, qbase);
     const bool more = it + 1 < n_iter;
-    if (more) {
-      const int h1 = kvh * grp + (it + 1) / per_head;
-      const int qb1 = (qt0 + (it + 1) % per_head) * BQ;
-      ql.load(Q, dO, q_stride, o_stride, LSE, delta, b, h1, S, Hq, qb1, tid);
-    }
+    if (more) stage(it + 1, cur ^ 1);
+    const char* qs = smem + SM::Q_OFF + cur * SM::TILE_Q;
+    const char* dos = smem + SM::DO_OFF + cur * SM::TILE_Q;
+    const float* lse_s = reinterpret_cast<const float*>(smem + SM::LSE_OFF + cur * BQ * 4);
+    const float* del_s = reinterpret_cast<const float*>(smem + SM::DEL_OFF + cur * BQ * 4);
 
-    // ---- S = Q K^T, dP = dO V^T (lane owns key `mykey`) ----
-    f32x16 sacc[QBS], pacc[QBS];
-#pragma unroll
-    for (int qb = 0; qb < QBS; ++qb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        sacc[qb][r] = 0.f;
-        pacc[qb][r] = 0.f;
-      }
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-#pragma unroll
-      for (int qb = 0; qb < QBS; ++qb) {
-        const int r = qb * 32 + lrow;
-        const half8 qa = as_half8(*reinterpret_cast<const u32x4*>(
-            smem + SM::Q_OFF + r * SM::ROW_B + cswz(r, kk * 2 + g) * 16));
-        const half8 da = as_half8(*reinterpret_cast<const u32x4*>(
-            smem + SM::DO_OFF + r * SM::ROW_B + cswz(r, kk * 2 + g) * 16));
-        sacc[qb] = mfma32(qa, kf[kk], sacc[qb]);
-        pacc[qb] = mfma32(da, vf[kk], pacc[qb]);
-      }
-    }
-
-    // ---- P = exp(scale s - LSE), dS = P (dP - D) ----
-    half8 pp[QBS][2], pds[QBS][2];
+    // One 32-query half at a time (keeps the live accumulators small):
+    //   S = Q K^T, dP = dO V^T          (lane owns key `mykey`, 16 query rows)
+    //   P = exp2(s*scale*log2e - LSE2), dS = P (dP - D)
+    //   dS^T -> LDS;  dV^T += dO^T P,  dK^T += Q^T dS
+    // (queries past S have zero Q and dO rows and zero LSE2 and D: finite P,
+    // zero dS and zero contributions)
     const bool need_mask = (causal && kw0 + 31 > qbase) || kw0 + 32 > S;
+    const int keyl = wave * 32 + lrow;
 #pragma unroll
     for (int qb = 0; qb < QBS; ++qb) {
+      f32x16 sacc, pacc;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        sacc[r] = 0.f;
+        pacc[r] = 0.f;
+      }
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        sacc = mfma32(RT::row_frag(qs, qb * 32, kk, lane), kf[kk], sacc);
+        pacc = mfma32(RT::row_frag(dos, qb * 32, kk, lane), vf[kk], pacc);
+      }
+
       float p[16], ds[16];
 #pragma unroll
       for (int rq = 0; rq < 4; ++rq) {
@@ -317,52 +296,51 @@ attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = 4 * rq + e;
-          float pv = fast_exp2(fmaf(sacc[qb][r], c, -lv[e]));
-          if (need_mask) {
-            const int q = qbase + ql0 + e;
-            if ((causal && mykey > q) || mykey >= S) pv = 0.f;
-          }
-          p[r] = pv;
-          ds[r] = pv * (pacc[qb][r] - dv[e]);
+          p[r] = fast_exp2(fmaf(sacc[r], c, -lv[e]));
+          ds[r] = pacc[r] - dv[e];
         }
       }
+      if (need_mask) {   // wave-uniform: diagonal or ragged key tile
+        // key > query (causal) or key past S -> P = 0
+        const int qlim = causal ? mykey : 0;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int q = qbase + qb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+          const bool masked = (q < qlim) | (mykey >= S);
+          p[r] = masked ? 0.f : p[r];
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) ds[r] *= p[r];
+      half8 pp[2], pds[2];
 #pragma unroll
       for (int kc = 0; kc < 2; ++kc) {
-        pp[qb][kc] = pack8(p[8 * kc], p[8 * kc + 1], p[8 * kc + 2], p[8 * kc + 3], p[8 * kc + 4],
-                           p[8 * kc + 5], p[8 * kc + 6], p[8 * kc + 7]);
-        pds[qb][kc] = pack8(ds[8 * kc], ds[8 * kc + 1], ds[8 * kc + 2], ds[8 * kc + 3],
-                            ds[8 * kc + 4], ds[8 * kc + 5], ds[8 * kc + 6], ds[8 * kc + 7]);
+        pp[kc] = pack8(p[8 * kc], p[8 * kc + 1], p[8 * kc + 2], p[8 * kc + 3], p[8 * kc + 4],
+                       p[8 * kc + 5], p[8 * kc + 6], p[8 * kc + 7]);
+        pds[kc] = pack8(ds[8 * kc], ds[8 * kc + 1], ds[8 * kc + 2], ds[8 * kc + 3],
+                        ds[8 * kc + 4], ds[8 * kc + 5], ds[8 * kc + 6], ds[8 * kc + 7]);
       }
-      // dS -> LDS [query][key] for dQ
-      const int keyl = wave * 32 + lrow;
+      // dS^T row `keyl`, queries ql0..ql0+3 (8 bytes) for each 4-run
 #pragma unroll
-      for (int kc = 0; kc < 2; ++kc)
+      for (int rq = 0; rq < 4; ++rq) {
+        const int ql0 = qb * 32 + 8 * rq + 4 * g;
+        const half8& src = pds[rq >> 1];
+        half4 d4h;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int r = 8 * kc + e;
-          const int q = qb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
-          *reinterpret_cast<_Float16*>(smem + SM::DS_OFF + q * SM::DS_ROWB +
-                                       cswz(q, keyl >> 3) * 16 + (keyl & 7) * 2) = pds[qb][kc][e];
-        }
-    }
-
-    // ---- dV^T += dO^T P,  dK^T += Q^T dS ----
+        for (int e = 0; e < 4; ++e) d4h[e] = src[4 * (rq & 1) + e];
+        *reinterpret_cast<half4*>(smem + SM::DST_OFF + dst_off(keyl, ql0)) = d4h;
+      }
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const int r = db * 32 + lrow;
-#pragma unroll
-      for (int qb = 0; qb < QBS; ++qb)
+      for (int db = 0; db < DB; ++db)
 #pragma unroll
         for (int kc = 0; kc < 2; ++kc) {
-          const half8 doT = ld_perm8(smem + SM::DOT_OFF + r * SM::QT_ROWB, r, qb * 32 + kc * 16, g);
-          const half8 qT = ld_perm8(smem + SM::QT_OFF + r * SM::QT_ROWB, r, qb * 32 + kc * 16, g);
-          dvacc[db] = mfma32(doT, pp[qb][kc], dvacc[db]);
-          dkacc[db] = mfma32(qT, pds[qb][kc], dkacc[db]);
+          const int kb = qb * 32 + kc * 16;
+          dvacc[db] = mfma32(RT::template tr_frag<true>(dos, kb, db * 32, lane), pp[kc], dvacc[db]);
+          dkacc[db] = mfma32(RT::template tr_frag<true>(qs, kb, db * 32, lane), pds[kc], dkacc[db]);
         }
     }
 
-    __syncthreads();   // dS complete; Q-side tiles no longer read
-    if (more) ql.store(smem, tid);
+    __syncthreads();   // dS^T complete
 
     // ---- dQ (partial over this workgroup's keys) = dS K -> atomics ----
     // Result lane layout: column d (one per lane), rows q in 4-runs, so each
@@ -375,24 +353,40 @@ attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
       f32x16 acc;
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-      const int kr = db * 32 + lrow;
-      const int qr = qb * 32 + lrow;
 #pragma unroll
       for (int kc = 0; kc < BKV / 16; ++kc) {
-        const half8 ka = as_half8(*reinterpret_cast<const u32x4*>(
-            smem + SM::KT_OFF + kr * SM::KT_ROWB + cswz(kr, kc * 2 + g) * 16));
-        const half8 sa = as_half8(*reinterpret_cast<const u32x4*>(
-            smem + SM::DS_OFF + qr * SM::DS_ROWB + cswz(qr, kc * 2 + g) * 16));
-        acc = mfma32(sa, ka, acc);
+        // dS as A: rows q (qb*32 + lane%32), keys kc*16 + 8*(lane/32) + 0..7,
+        // read transposed from dS^T[key][q]
+        const int q = qb * 32 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+        v4s part[2];
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const int key = kc * 16 + 8 * (lane >> 5) + 4 * hh + ((lane & 15) >> 2);
+          part[hh] = lds_read_tr16(smem + SM::DST_OFF + dst_off(key, q));
+        }
+        const half8 sa = as_half8(pack_v4s_pair(part[0], part[1]));
+        const half8 kb = RT::template tr_frag<false>(smem + SM::K_OFF, kc * 16, db * 32, lane);
+        acc = mfma32(sa, kb, acc);
       }
-      float* dst = dq_acc + ((int64_t)b * S * Hq + h) * D + db * 32 + lrow;
+      // rows qbase + qb*32 + 0..31 of this head; rows past S are outside the
+      // buffer and their atomics are dropped
+      const int q0 = qbase + qb * 32;
+      const int nv = S - q0 < 32 ? S - q0 : 32;
+      const int rowb = Hq * D * 4;
+      const rsrc_t rs = make_rsrc(dq_acc + (((int64_t)b * S + q0) * Hq + h) * D,
+                                  nv > 0 ? (uint32_t)(nv * rowb) : 0u);
+      const uint32_t lane_off = (uint32_t)((4 * g * Hq * D + db * 32 + lrow) * 4);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int q = qbase + qb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
-        if (q < S) unsafeAtomicAdd(dst + (int64_t)q * Hq * D, acc[r]);
+        const uint32_t off = lane_off + (uint32_t)((8 * (r >> 2) + (r & 3)) * rowb);
+        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(acc[r], rs, (int)off, 0, 0);
       }
     }
-    __syncthreads();   // next tile's Q-side data visible; dS reads done
+
+    // own direct loads of the next tile are done (only the dQ atomics may
+    // still be in flight), then everyone's are
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(DQ_BLK * 16) : "memory");
+    __syncthreads();
   }
 
   // ---- write dK = scale * acc, dV ----
@@ -443,13 +437,13 @@ hipError_t launch_bwd(const AttnBwdArgs& a, hipStream_t s) {
   const int64_t threads = rows * (D / 8);
   const unsigned eblocks = (unsigned)((threads + 255) / 256);
   hipLaunchKernelGGL((attn_bwd_pre_kernel<D>), dim3(eblocks), dim3(256), 0, s, a.O, a.dO,
-                     a.o_stride, a.delta, a.dq_acc, sh.B, sh.S, sh.Hq);
+                     a.o_stride, a.LSE, a.delta, a.lse2, a.dq_acc, sh.B, sh.S, sh.Hq);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int n_kt = (sh.S + BKV - 1) / BKV;
   hipLaunchKernelGGL((attn_bwd_main_kernel<D>), dim3((unsigned)(n_kt * sh.B * sh.Hkv)),
                      dim3(NW * 64), 0, s, a.Q, a.K, a.V, a.q_stride, a.kv_stride, a.dO, a.o_stride,
-                     a.LSE, a.delta, a.dq_acc, a.dK, a.dV, a.dkv_stride, sh.B, sh.S, sh.Hq, sh.Hkv,
+                     a.lse2, a.delta, a.dq_acc, a.dK, a.dV, a.dkv_stride, sh.B, sh.S, sh.Hq, sh.Hkv,
                      sh.scale, sh.causal);
   e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -87,6 +87,42 @@ __device__ __forceinline__ void lds_dma16(rsrc_t r, void* lds, uint32_t voff, ui
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (LT_LDS void*)lds, 16, (int)voff, (int)soff, 0, 0);
 }
 
+// Same load, issued as an opaque instruction pair (M0 = LDS address, then the
+// buffer load).  The compiler does not see the LDS write, so it adds no
+// conservative vmcnt wait before later LDS reads of *other* buffers; the
+// caller orders the data with an explicit s_waitcnt vmcnt + barrier.  Raw
+// buffer descriptor: 48-bit base, stride 0, num_records bytes.
+__device__ __forceinline__ void lds_dma16_opaque(const void* base, uint32_t nrec, void* lds,
+                                                 uint32_t voff) {
+  const uint64_t b = (uint64_t)base;
+  u32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((uint32_t)b);
+  r[1] = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32) & 0xffffu);
+  r[2] = __builtin_amdgcn_readfirstlane(nrec);
+  r[3] = 0x00020000u;
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(m0v), "v"(voff), "s"(r)
+               : "memory");
+}
+
+// 4 bytes per lane (lane l's dword lands at lds + 4*l); otherwise as above.
+__device__ __forceinline__ void lds_dma4_opaque(const void* base, uint32_t nrec, void* lds,
+                                                uint32_t voff) {
+  const uint64_t b = (uint64_t)base;
+  u32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((uint32_t)b);
+  r[1] = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32) & 0xffffu);
+  r[2] = __builtin_amdgcn_readfirstlane(nrec);
+  r[3] = 0x00020000u;
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+               :
+               : "s"(m0v), "v"(voff), "s"(r)
+               : "memory");
+}
+
 // ds_read_b64_tr_b16: within each 16-lane group, lane l receives element
 // (l % 4) of the 8-byte chunks read by lanes (l/4) + 4q, q = 0..3.
 __device__ __forceinline__ v4s lds_read_tr16(const void* p) {

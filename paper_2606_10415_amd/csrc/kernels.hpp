@@ -55,7 +55,8 @@ struct AttnBwdArgs {
   lt_half* dK;
   lt_half* dV;
   int64_t dq_stride, dkv_stride;
-  float* delta;   // workspace: [B, Hq, S]
+  float* delta;   // workspace: [B, Hq, S]  rowsum(dO * O)
+  float* lse2;    // workspace: [B, Hq, S]  LSE * log2(e)
   float* dq_acc;  // workspace: [B, S, Hq, D]
 };
 
@@ -64,6 +65,7 @@ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 inline size_t attn_bwd_delta_bytes(int B, int S, int Hq) {
   return align256((size_t)B * Hq * S * sizeof(float));
 }
+inline size_t attn_bwd_lse2_bytes(int B, int S, int Hq) { return attn_bwd_delta_bytes(B, S, Hq); }
 inline size_t attn_bwd_dq_bytes(int B, int S, int Hq, int D) {
   return align256((size_t)B * S * Hq * D * sizeof(float));
 }

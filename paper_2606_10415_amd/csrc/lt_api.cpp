@@ -136,7 +136,8 @@ lt_status lt_attn_fwd(const lt_half* Q, const lt_half* K, const lt_half* V, int6
 
 size_t lt_attn_bwd_workspace_size(int B, int S, int Hq, int Hkv, int D) {
   if (B < 1 || S < 1 || Hq < 1 || Hkv < 1 || D < 1 || Hq % Hkv) return 0;
-  return lt::attn_bwd_delta_bytes(B, S, Hq) + lt::attn_bwd_dq_bytes(B, S, Hq, D);
+  return lt::attn_bwd_delta_bytes(B, S, Hq) + lt::attn_bwd_lse2_bytes(B, S, Hq) +
+         lt::attn_bwd_dq_bytes(B, S, Hq, D);
 }
 
 lt_status lt_attn_bwd(const lt_half* Q, const lt_half* K, const lt_half* V, int64_t q_row_stride,
@@ -169,7 +170,9 @@ lt_status lt_attn_bwd(const lt_half* Q, const lt_half* K, const lt_half* V, int6
                     Q, K, V, q_row_stride, kv_row_stride, O, dO, o_row_stride, LSE, dQ, dK, dV,
                     dq_row_stride, dkv_row_stride,
                     reinterpret_cast<float*>(ws),
-                    reinterpret_cast<float*>(ws + lt::attn_bwd_delta_bytes(B, S, Hq))};
+                    reinterpret_cast<float*>(ws + lt::attn_bwd_delta_bytes(B, S, Hq)),
+                    reinterpret_cast<float*>(ws + lt::attn_bwd_delta_bytes(B, S, Hq) +
+                                             lt::attn_bwd_lse2_bytes(B, S, Hq))};
   return from_hip(lt::attn_bwd_launch(a, reinterpret_cast<hipStream_t>(stream)), "attn_bwd launch");
 }
 
