@@ -78,15 +78,15 @@ attn_bwd_pre_kernel(const lt_half* __restrict__ O, const lt_half* __restrict__ d
 
 // ------------------------------------------------------------ kernel 2
 // Row-layout tile [rows][D] (features contiguous), 2D bytes per row; the
-// 16-byte chunk c of row r sits at chunk c ^ gsw(r).  gsw spreads eight
-// consecutive rows over eight chunk positions (conflict-free row reads) and
-// four consecutive rows over four 64-byte windows (conflict-free transpose
-// reads).
+// 16-byte chunk c of row r sits at chunk c ^ gsw(r).  For 256-byte rows gsw
+// spreads sixteen consecutive rows over sixteen chunk positions (row reads:
+// 16 lanes x 16 B per LDS cycle) and four consecutive rows over four 64-byte
+// windows (transpose reads).
 template <int D>
 struct RowTile {
   static constexpr int CPR = D / 8;       // 16-byte chunks per row
   static constexpr int ROWB = 2 * D;
-  __device__ static __forceinline__ int gsw(int r) { return ((r & 7) ^ ((r & 3) << 2)) & (CPR - 1); }
+  __device__ static __forceinline__ int gsw(int r) { return ((r & 15) ^ ((r & 3) << 2)) & (CPR - 1); }
   __device__ static __forceinline__ int addr(int r, int c) { return r * ROWB + ((c ^ gsw(r)) << 4); }
 
   // Direct loads of ROWS rows starting at global row pointer g (row stride

@@ -20,7 +20,8 @@
 //     LDS transpose read (ds_read_b64_tr_b16), so every (transA, transB)
 //     runs the same MFMA loop at the same speed;
 //   * LDS positions are XOR-swizzled so that both the direct loads and the
-//     MFMA operand reads are free of bank conflicts;
+//     MFMA operand reads are free of bank conflicts (16 lanes x 16 B per LDS
+//     cycle);
 //   * tiles are ordered so that each XCD gets a contiguous range of tiles,
 //     grouped eight tile-rows at a time for L2 reuse of A and B.
 //   Buffer loads return zeros out of range, which provides the M, N and K
@@ -35,7 +36,8 @@ constexpr int BK = 64;   // K slice (halves)
 
 // One operand tile: R rows (M for A, N for B) x BK.
 //   KC  (K-contiguous in HBM): LDS row-major, 128 B per row; 16-byte chunk c
-//       of row r sits at position c ^ (r & 7).
+//       of row r sits at position c ^ ((r >> 1) & 7), so the 16 rows that one
+//       LDS cycle serves (16 lanes x 16 B) land in 16 different bank groups.
 //   !KC (row index contiguous in HBM): LDS k-major, 2R bytes per k-row;
 //       16-byte chunk c (rows 8c..8c+7) of k-row k sits at position
 //       ((c >> 2) ^ (k & 3)) * 4 + (c & 3).
@@ -65,7 +67,7 @@ struct Operand {
 #pragma unroll
       for (int t = 0; t < PERW; ++t) {
         const int r = (wave * PERW + t) * 8 + lane / 8;
-        const int c = (lane % 8) ^ (r & 7);
+        const int c = (lane % 8) ^ ((r >> 1) & 7);
         voff[t] = (uint32_t)((r * ld + c * 8) * 2);
       }
     } else {
@@ -91,7 +93,7 @@ struct Operand {
         uint32_t off = voff[t];
         if (kvalid < BK) {
           const int r = n * 8 + lane / 8;
-          if (((lane % 8) ^ (r & 7)) * 8 >= kvalid) off = kOOB;
+          if (((lane % 8) ^ ((r >> 1) & 7)) * 8 >= kvalid) off = kOOB;
         }
         lds_dma16(rs, lds + n * 1024, off, (uint32_t)(k0 * 2));
       }
@@ -113,7 +115,7 @@ struct Operand {
     if constexpr (KC) {
       const int r = rb + (lane & 31);
       const int c = kk * 2 + (lane >> 5);
-      return as_half8(*reinterpret_cast<const u32x4*>(lds + r * 128 + ((c ^ (r & 7)) << 4)));
+      return as_half8(*reinterpret_cast<const u32x4*>(lds + r * 128 + ((c ^ ((r >> 1) & 7)) << 4)));
     } else {
       // Two transpose reads (h = 0, 1).  Lane L reads 4 rows at
       // m = rb + 16*((L/16)%2) + 4*(L%4) of k-row kk*16 + 8*(L/32) + 4h + (L%16)/4,
@@ -201,42 +203,54 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
+  if (nk > 0) frag_load(smem, 0, 0);
+
+  // Per slice: the next slice's direct loads go out first; MFMA step kk runs
+  // on fragments loaded during step kk-1.  The barrier sits before the last
+  // step, whose fragments are already in registers, so that the first
+  // fragments of the next slice are read while that step's MFMAs execute.
+  constexpr int KS = BK / 16;
+  auto mfma_step = [&](int s) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(fb[s][j], fa[s][i], acc[i][j]);
+  };
+  auto interleave = [&]() {
+    // pair this step's MFMAs with the next step's LDS reads
+    constexpr int NRD = (TA ? 2 : 1) * TM + (TB ? 1 : 2) * TN;
+    constexpr int NMF = TM * TN;
+    constexpr int NPAIR = NRD < NMF ? NRD : NMF;
+#pragma unroll
+    for (int t = 0; t < NPAIR; ++t) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    if (NMF > NPAIR) __builtin_amdgcn_sched_group_barrier(0x008, NMF - NPAIR, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
 
   for (int kt = 0; kt < nk; ++kt) {
     char* cur = smem + (kt & 1) * STAGE;
     char* nxt = smem + ((kt + 1) & 1) * STAGE;
-    // next slice in flight while this one is consumed; its buffer was last
-    // read before the previous barrier
-    if (kt + 1 < nk) {
+    const bool more = kt + 1 < nk;
+    // its buffer was last read before the previous barrier
+    if (more) {
       oa.load(nxt, (int64_t)(kt + 1) * BK, kvalid(kt + 1), wave, lane);
       ob.load(nxt + OA::BYTES, (int64_t)(kt + 1) * BK, kvalid(kt + 1), wave, lane);
     }
-    frag_load(cur, 0, 0);
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      const int s = kk & 1;
-      if (kk + 1 < BK / 16) frag_load(cur, kk + 1, s ^ 1);
-      // D[n][m] = sum_k B^T[n][k] A^T[k][m]: lane holds column m, 4-runs of n
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(fb[s][j], fa[s][i], acc[i][j]);
-      if (kk + 1 < BK / 16) {
-        // interleave the next step's LDS reads with this step's MFMAs
-        constexpr int NRD = (TA ? 2 : 1) * TM + (TB ? 1 : 2) * TN;
-        constexpr int NMF = TM * TN;
-        constexpr int NPAIR = NRD < NMF ? NRD : NMF;
-#pragma unroll
-        for (int t = 0; t < NPAIR; ++t) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        }
-        if (NMF > NPAIR) __builtin_amdgcn_sched_group_barrier(0x008, NMF - NPAIR, 0);
-        __builtin_amdgcn_sched_barrier(0);
-      }
+    for (int kk = 0; kk < KS - 1; ++kk) {
+      frag_load(cur, kk + 1, (kk + 1) & 1);
+      mfma_step(kk & 1);
+      interleave();
     }
+    // next slice resident for all waves; nobody reads `cur` after this point
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+    if (more) frag_load(nxt, 0, 0);
+    mfma_step((KS - 1) & 1);
+    if (more) interleave();
   }
 
   // ---- epilogue: C[m][n..n+3] = alpha * acc + beta * R[m][n..n+3] ----
