@@ -14,6 +14,7 @@ attention backward) divided by the measured step time.
 """
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -29,6 +30,36 @@ from paper_2606_10415_amd.synth import WORKLOADS, layer_inputs  # noqa: E402
 
 PEAK_FP16_TFLOPS = 2516.6     # MI355X dense FP16 MFMA (256 CU x 2.4 GHz x 4096 FLOP/clk)
 PEAK_HBM_GBS = 8000.0
+
+# HBM traffic of the GEMM kernel at llama2-7b: mean bytes per launch over the 12
+# GEMM launches of one layer step, from two rocprofv3 --pmc runs of this script
+# (FETCH_SIZE, then WRITE_SIZE, with --copy-calibration-mib 1024) each scaled by
+# what the same counter reads for the calibration copy of known size.  The
+# figure holds only for the kernel sources it was measured on: any change to
+# them makes bench report traffic as null until the counters are taken again.
+GEMM_TRAFFIC = {
+    "workload": "llama2-7b",
+    "sources_sha256": "dcf1211fae4fc600dde8ec2bf0ae5a50069d2c8c0b3f66d321de9d2433ebe563",
+    "fetch_bytes_per_launch": 691088867,
+    "write_bytes_per_launch": 88791967,
+}
+GEMM_SOURCES = ("paper_2606_10415_amd/csrc/gemm_f16.hip", "paper_2606_10415_amd/csrc/common.hpp")
+
+
+def gemm_sources_sha256():
+    h = hashlib.sha256()
+    for rel in GEMM_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def gemm_traffic(w):
+    t = GEMM_TRAFFIC
+    if (t["sources_sha256"] is None or t["workload"] != w.name
+            or t["sources_sha256"] != gemm_sources_sha256()):
+        return None
+    return int(t["fetch_bytes_per_launch"] + t["write_bytes_per_launch"])
 
 
 def layer_flops(w):
@@ -95,6 +126,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama2-7b", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="before warmup, run a plain elementwise copy (negation) of this many "
+                         "MiB of fp16 three times: the reference dispatch for scaling HBM "
+                         "byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU (its layer at full shape); --gpus {args.gpus} is not "
@@ -111,6 +146,17 @@ def main():
     L = DecoderLayer(w, layer_inputs(w))
     stream = torch.cuda.current_stream()
     fl = layer_flops(w)
+
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib * (1 << 20) // 2
+        src = torch.empty(n, dtype=torch.float16, device="cuda").normal_()
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        print(f"[bench] calibration copy: {n * 2} bytes read and {n * 2} written per dispatch",
+              file=sys.stderr, flush=True)
+        del src, dst
 
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
@@ -141,6 +187,14 @@ def main():
     ms_total = start.elapsed_time(end)
     ms_per_step = ms_total / args.steps
 
+    step_ms = []
+    step_start = None
+    for name, ev in events + [("__step__", end)]:
+        if name == "__step__":
+            if step_start is not None:
+                step_ms.append(step_start.elapsed_time(ev))
+            step_start = ev
+
     per_op = {}
     prev = None
     for name, ev in events:
@@ -164,6 +218,9 @@ def main():
         "swiglu_fwd_ms": round(avg["swiglu_fwd"], 4), "swiglu_bwd_ms": round(avg["swiglu_bwd"], 4),
         "swiglu_fwd_gbs": round(6 * w.T * w.F / (avg["swiglu_fwd"] * 1e-3) / 1e9, 1),
         "swiglu_bwd_gbs": round(10 * w.T * w.F / (avg["swiglu_bwd"] * 1e-3) / 1e9, 1),
+        "step_ms_median": round(float(np.median(step_ms)), 4),
+        "step_ms_min": round(float(np.min(step_ms)), 4),
+        "step_ms_max": round(float(np.max(step_ms)), 4),
         "per_op_ms": {k: round(v, 4) for k, v in avg.items()},
         "wall_s": round(wall, 3),
     }
@@ -194,7 +251,7 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "gemm_f16 (12 launches per step)",
                      "achieved": round(gemm_tflops, 1), "peak": PEAK_FP16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK_FP16_TFLOPS, 4),
-                     "traffic": None},
+                     "traffic": gemm_traffic(w)},
         "attn_bwd": {"achieved": round(attn_bwd_tflops, 1), "peak": PEAK_FP16_TFLOPS,
                      "frac": round(attn_bwd_tflops / PEAK_FP16_TFLOPS, 4)},
         "cpu_baseline": cpu,
