@@ -32,23 +32,29 @@
 namespace lt {
 namespace {
 
-constexpr int BK = 64;   // K slice (halves)
-
 // One operand tile: R rows (M for A, N for B) x BK.
-//   KC  (K-contiguous in HBM): LDS row-major, 128 B per row; 16-byte chunk c
-//       of row r sits at position c ^ ((r >> 1) & 7), so the 16 rows that one
-//       LDS cycle serves (16 lanes x 16 B) land in 16 different bank groups.
+//   KC  (K-contiguous in HBM): LDS row-major, CPR = BK/8 16-byte chunks per
+//       row; chunk c of row r sits at position c ^ swz(r), which places the
+//       16 consecutive rows read by one LDS cycle (16 lanes x 16 B) in 16
+//       different bank groups.
 //   !KC (row index contiguous in HBM): LDS k-major, 2R bytes per k-row;
 //       16-byte chunk c (rows 8c..8c+7) of k-row k sits at position
 //       ((c >> 2) ^ (k & 3)) * 4 + (c & 3).
-template <int R, bool KC, int NT>
+// Both are filled by direct global -> LDS loads issued as opaque
+// instructions, so the caller orders them with explicit vmcnt waits.
+template <int R, int BK, bool KC, int NT>
 struct Operand {
   static constexpr int BYTES = R * BK * 2;
   static constexpr int NINST = BYTES / 1024;        // 1 KiB direct loads per slice
   static constexpr int PERW = NINST / (NT / 64);     // ... per wave
   static_assert(NINST % (NT / 64) == 0, "slice must split across waves");
+  static constexpr int CPR = BK / 8;                 // KC: 16-byte chunks per row
+  static constexpr int RPI = 64 / CPR;               // KC: rows per direct load
   static constexpr int KR_PER = 1024 / (2 * R);      // !KC: k-rows per direct load
   static constexpr int LPR = 64 / KR_PER;            // !KC: lanes per k-row
+  static_assert(CPR >= 4 && CPR <= 16, "KC layout needs 32 <= BK <= 128");
+
+  __device__ static __forceinline__ int swz(int r) { return (r / (16 / CPR)) & (CPR - 1); }
 
   uint32_t voff[PERW];
   const lt_half* base;
@@ -66,8 +72,8 @@ struct Operand {
       nrec = (uint32_t)(nvalid * ld * 2);
 #pragma unroll
       for (int t = 0; t < PERW; ++t) {
-        const int r = (wave * PERW + t) * 8 + lane / 8;
-        const int c = (lane % 8) ^ ((r >> 1) & 7);
+        const int r = (wave * PERW + t) * RPI + lane / CPR;
+        const int c = (lane % CPR) ^ swz(r);
         voff[t] = (uint32_t)((r * ld + c * 8) * 2);
       }
     } else {
@@ -86,25 +92,28 @@ struct Operand {
   // kvalid < BK only for the last slice of a ragged K.
   __device__ __forceinline__ void load(char* lds, int64_t k0, int kvalid, int wave, int lane) const {
     if constexpr (KC) {
-      const rsrc_t rs = make_rsrc(base + row0 * ld, nrec);
+      // descriptor based at column k0 of row row0: the range shrinks by the
+      // same 2*k0 bytes, so rows past the matrix still read as zero
+      const lt_half* b = base + row0 * ld + k0;
+      const uint32_t n = nrec - (uint32_t)(k0 * 2);
 #pragma unroll
       for (int t = 0; t < PERW; ++t) {
-        const int n = wave * PERW + t;
+        const int i = wave * PERW + t;
         uint32_t off = voff[t];
         if (kvalid < BK) {
-          const int r = n * 8 + lane / 8;
-          if (((lane % 8) ^ ((r >> 1) & 7)) * 8 >= kvalid) off = kOOB;
+          const int r = i * RPI + lane / CPR;
+          if (((lane % CPR) ^ swz(r)) * 8 >= kvalid) off = kOOB;
         }
-        lds_dma16(rs, lds + n * 1024, off, (uint32_t)(k0 * 2));
+        lds_dma16_opaque(b, n, lds + i * 1024, off);
       }
     } else {
-      const rsrc_t rs = make_rsrc(base + k0 * ld + row0, nrec);
+      const lt_half* b = base + k0 * ld + row0;
 #pragma unroll
       for (int t = 0; t < PERW; ++t) {
-        const int n = wave * PERW + t;
+        const int i = wave * PERW + t;
         uint32_t off = voff[t];
-        if (kvalid < BK && n * KR_PER + lane / LPR >= kvalid) off = kOOB;
-        lds_dma16(rs, lds + n * 1024, off, 0);
+        if (kvalid < BK && i * KR_PER + lane / LPR >= kvalid) off = kOOB;
+        lds_dma16_opaque(b, nrec, lds + i * 1024, off);
       }
     }
   }
@@ -115,7 +124,7 @@ struct Operand {
     if constexpr (KC) {
       const int r = rb + (lane & 31);
       const int c = kk * 2 + (lane >> 5);
-      return as_half8(*reinterpret_cast<const u32x4*>(lds + r * 128 + ((c ^ ((r >> 1) & 7)) << 4)));
+      return as_half8(*reinterpret_cast<const u32x4*>(lds + r * (CPR * 16) + ((c ^ swz(r)) << 4)));
     } else {
       // Two transpose reads (h = 0, 1).  Lane L reads 4 rows at
       // m = rb + 16*((L/16)%2) + 4*(L%4) of k-row kk*16 + 8*(L/32) + 4h + (L%16)/4,
@@ -135,7 +144,22 @@ struct Operand {
   }
 };
 
-template <int BM, int BN, int WGM, int WGN, bool TA, bool TB>
+// s_waitcnt vmcnt(n * PER), n clamped to [0, MAXN]: wait until at most n
+// slices of direct loads (PER instructions each) are still in flight.
+template <int PER, int MAXN>
+__device__ __forceinline__ void wait_slices(int n) {
+  if constexpr (MAXN > 0) {
+    if (n >= MAXN) {
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(MAXN * PER) : "memory");
+      return;
+    }
+    wait_slices<PER, MAXN - 1>(n);
+  } else {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
+}
+
+template <int BM, int BN, int WGM, int WGN, int BK, int NS, bool TA, bool TB>
 __global__ void __launch_bounds__(WGM * WGN * kWave)
 gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
                 const lt_half* __restrict__ A, int64_t lda,
@@ -145,10 +169,12 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   constexpr int NT = WGM * WGN * kWave;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;   // wave tile
   constexpr int TM = WTM / 32, TN = WTN / 32;     // 32x32 MFMA blocks per wave
-  using OA = Operand<BM, !TA, NT>;
-  using OB = Operand<BN, TB, NT>;
+  using OA = Operand<BM, BK, !TA, NT>;
+  using OB = Operand<BN, BK, TB, NT>;
   constexpr int STAGE = OA::BYTES + OB::BYTES;
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+  constexpr int PER_SLICE = OA::PERW + OB::PERW;  // direct loads per wave per slice
+  static_assert(NS >= 2 && (NS - 2) * PER_SLICE <= 63, "vmcnt range");
+  __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -189,6 +215,12 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
     const int64_t rem = K - (int64_t)kt * BK;
     return rem >= BK ? BK : (int)rem;
   };
+  auto stage_of = [&](int kt) { return smem + (kt % NS) * STAGE; };
+  auto issue = [&](int kt) {
+    char* st = stage_of(kt);
+    oa.load(st, (int64_t)kt * BK, kvalid(kt), wave, lane);
+    ob.load(st + OA::BYTES, (int64_t)kt * BK, kvalid(kt), wave, lane);
+  };
   half8 fa[2][TM], fb[2][TN];
   auto frag_load = [&](const char* st, int kk, int s) {
 #pragma unroll
@@ -197,18 +229,19 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
     for (int j = 0; j < TN; ++j) fb[s][j] = ob.frag(st + OA::BYTES, wn * WTN + j * 32, kk, lane);
   };
 
-  if (nk > 0) {
-    oa.load(smem, 0, kvalid(0), wave, lane);
-    ob.load(smem + OA::BYTES, 0, kvalid(0), wave, lane);
-  }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  // ---- prologue: slices 0 .. NS-2 in flight, wait for slice 0 ----
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < nk) issue(s);
+  wait_slices<PER_SLICE, NS - 2>(min(NS - 2, nk - 1));
   __syncthreads();
   if (nk > 0) frag_load(smem, 0, 0);
 
-  // Per slice: the next slice's direct loads go out first; MFMA step kk runs
-  // on fragments loaded during step kk-1.  The barrier sits before the last
-  // step, whose fragments are already in registers, so that the first
-  // fragments of the next slice are read while that step's MFMAs execute.
+  // Per slice kt: the loads of slice kt+NS-1 go out first (into the stage
+  // that slice kt-1 used); MFMA step kk runs on fragments read during step
+  // kk-1.  The barrier sits before the last step, whose fragments are already
+  // in registers, so that the first fragments of slice kt+1 are read while
+  // that step's MFMAs execute.
   constexpr int KS = BK / 16;
   auto mfma_step = [&](int s) {
 #pragma unroll
@@ -231,24 +264,21 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   };
 
   for (int kt = 0; kt < nk; ++kt) {
-    char* cur = smem + (kt & 1) * STAGE;
-    char* nxt = smem + ((kt + 1) & 1) * STAGE;
-    const bool more = kt + 1 < nk;
-    // its buffer was last read before the previous barrier
-    if (more) {
-      oa.load(nxt, (int64_t)(kt + 1) * BK, kvalid(kt + 1), wave, lane);
-      ob.load(nxt + OA::BYTES, (int64_t)(kt + 1) * BK, kvalid(kt + 1), wave, lane);
-    }
+    const char* cur = stage_of(kt);
+    // its stage was last read before the previous iteration's barrier
+    if (kt + NS - 1 < nk) issue(kt + NS - 1);
 #pragma unroll
     for (int kk = 0; kk < KS - 1; ++kk) {
       frag_load(cur, kk + 1, (kk + 1) & 1);
       mfma_step(kk & 1);
       interleave();
     }
-    // next slice resident for all waves; nobody reads `cur` after this point
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // slice kt+1 resident for all waves (later slices may stay in flight);
+    // nobody reads `cur` after this point
+    wait_slices<PER_SLICE, NS - 2>(min(kt + NS - 1, nk - 1) - (kt + 1));
     __syncthreads();
-    if (more) frag_load(nxt, 0, 0);
+    const bool more = kt + 1 < nk;
+    if (more) frag_load(stage_of(kt + 1), 0, 0);
     mfma_step((KS - 1) & 1);
     if (more) interleave();
   }
@@ -283,11 +313,11 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, bool TA, bool TB>
+template <int BM, int BN, int WGM, int WGN, int BK, int NS, bool TA, bool TB>
 hipError_t launch(const GemmArgs& g, hipStream_t s) {
   const int tiles_m = (int)((g.M + BM - 1) / BM);
   const int tiles_n = (int)((g.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_f16_kernel<BM, BN, WGM, WGN, TA, TB>), dim3(tiles_m * tiles_n),
+  hipLaunchKernelGGL((gemm_f16_kernel<BM, BN, WGM, WGN, BK, NS, TA, TB>), dim3(tiles_m * tiles_n),
                      dim3(WGM * WGN * kWave), 0, s, g.M, g.N, g.K, g.alpha, g.A, g.lda, g.B, g.ldb,
                      g.beta, g.R, g.ldr, g.C, g.ldc, tiles_m, tiles_n);
   return hipGetLastError();
@@ -298,8 +328,8 @@ hipError_t dispatch_tile(const GemmArgs& g, hipStream_t s) {
   // 256x256 tiles once there are about as many tiles as CUs; smaller
   // problems use 128x128 tiles so that more workgroups exist.
   const int64_t big_tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
-  if (big_tiles >= 192) return launch<256, 256, 2, 4, TA, TB>(g, s);
-  return launch<128, 128, 2, 2, TA, TB>(g, s);
+  if (big_tiles >= 192) return launch<256, 256, 2, 4, 64, 2, TA, TB>(g, s);
+  return launch<128, 128, 2, 2, 64, 2, TA, TB>(g, s);
 }
 
 }  // namespace
