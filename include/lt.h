@@ -135,9 +135,12 @@ lt_status lt_attn_fwd(const lt_half* Q, const lt_half* K, const lt_half* V,
 
 /*
  * Bytes of device workspace lt_attn_bwd needs: the per-row term
- * D_i = rowsum(dO_i * O_i) [B, Hq, S] FP32, the row LSE in base 2
- * [B, Hq, S] FP32 and the FP32 dQ accumulator [B, S, Hq, D], each 256-byte
- * aligned.  0 for invalid sizes.
+ * D_i = rowsum(dO_i * O_i) [B, Hq, S] FP32 and the row LSE in base 2
+ * [B, Hq, S] FP32, each 256-byte aligned; with grouped queries (Hq > Hkv)
+ * and few key/value heads also FP32 partial dK and dV sums
+ * [2][n][B, S, Hkv, D], where n divides Hq/Hkv (the query heads of a group
+ * are then split over n workgroups per key tile; the partials are summed in
+ * a fixed order, so results stay deterministic).  0 for invalid sizes.
  */
 size_t lt_attn_bwd_workspace_size(int B, int S, int Hq, int Hkv, int D);
 

@@ -7,27 +7,36 @@
 // Here P is rebuilt from the forward's row LSE, P = exp(scale q.k - LSE), and
 // SoftmaxBackward is GS = P * (GP - D) with D_i = rowsum(GO_i * O_i).
 //
-// Three kernels:
+// Three kernels (four with grouped queries), none with an atomic:
 //   1. attn_bwd_pre : D_i = rowsum(dO_i * O_i) (one 8/16-lane group per row,
-//                     shuffle reduction), LSE in base 2, and zeroing of the
-//                     FP32 dQ accumulator.  HBM-bound.
-//   2. attn_bwd_main: one workgroup per (batch, kv head, 128-key tile); the
-//                     4 waves own 32 keys each and keep K, V fragments and the
-//                     dK, dV accumulators in registers for the whole loop over
-//                     the GQA group's query heads and the causal query tiles
-//                     (the paper's GSM reduction of GV / GK becomes register
-//                     accumulation, and the GQA sum over query heads is the
-//                     same loop).  Q and dO tiles (64 queries) stream HBM ->
-//                     LDS by direct buffer loads, double-buffered one tile
-//                     ahead.  S = Q K^T and dP = dO V^T put one key per lane,
-//                     so P and dS feed the dV / dK MFMAs from registers; the
-//                     Q^T / dO^T operands of those MFMAs are read from the
-//                     same row-layout tiles with the LDS transpose read, in
-//                     the reduction order of the P / dS accumulators.  dS goes
-//                     to LDS once (as dS^T, 8-byte stores) for dQ = dS K, whose
-//                     FP32 partials are added to the workspace with coalesced
-//                     global atomics.
-//   3. attn_bwd_dq  : dQ = scale * accumulator -> FP16.  HBM-bound.
+//                     shuffle reduction) and the LSE in base 2.  HBM-bound.
+//   2. attn_bwd_dkdv: key-major.  One workgroup per (batch, kv head, 128-key
+//                     tile); each of the 4 waves owns 32 keys and keeps their
+//                     K fragments and the dK, dV accumulators in registers for
+//                     the whole loop over the GQA group's query heads and the
+//                     causal 32-query blocks (the paper's GSM reduction of
+//                     GV / GK becomes register accumulation, and the GQA sum
+//                     is the same loop).  V stays in LDS; Q, dO, LSE and D
+//                     blocks stream HBM -> LDS by direct loads, double-buffered.
+//                     S = Q K^T and dP = dO V^T put one key per lane, so P and
+//                     dS feed the dV / dK MFMAs from registers; their Q^T /
+//                     dO^T operands come from the same row-layout tiles through
+//                     the LDS transpose read, in the accumulators' query order.
+//                     With grouped queries and few kv heads the group's query
+//                     heads are split over several workgroups, whose FP32
+//                     partial dK, dV go to the workspace and are summed in a
+//                     fixed order by attn_bwd_dkdv_sum (kernel 4).
+//   3. attn_bwd_dq  : query-major, the forward's layout.  One workgroup per
+//                     (batch, head, 128-query tile); each wave owns 32 queries
+//                     (Q and dO fragments and the dQ accumulator in registers)
+//                     and walks the causal 64-key slices of K and V (direct
+//                     loads, double-buffered), recomputing S^T and dP^T with
+//                     one query per lane; dQ^T += K^T dS^T reads K^T through the
+//                     transpose read.  dQ is written once, in FP16.
+// Kernels 2 and 3 both recompute S and dP: seven contractions instead of
+// five, traded for no dQ atomics (whose traffic would exceed the whole
+// algorithmic byte count several times) and two waves per SIMD in each.
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "attn_tiles.hpp"
@@ -36,8 +45,10 @@ namespace lt {
 namespace {
 
 constexpr int NW = 4;          // waves per workgroup
-constexpr int BKV = 128;       // keys per workgroup (32 per wave)
-constexpr int BQ = 64;         // queries per inner tile
+constexpr int BKV = 128;       // dK/dV: keys per workgroup (32 per wave)
+constexpr int BQA = 32;        // dK/dV: queries per block
+constexpr int BQB = NW * 32;   // dQ: queries per workgroup (32 per wave)
+constexpr int BKB = 64;        // dQ: keys per slice
 constexpr float kLog2e = 1.4426950408889634f;
 
 // ------------------------------------------------------------ kernel 1
@@ -45,7 +56,7 @@ template <int D>
 __global__ void __launch_bounds__(256)
 attn_bwd_pre_kernel(const lt_half* __restrict__ O, const lt_half* __restrict__ dO, int64_t o_stride,
                     const float* __restrict__ LSE, float* __restrict__ delta,
-                    float* __restrict__ lse2, float* __restrict__ dq_acc, int B, int S, int Hq) {
+                    float* __restrict__ lse2, int B, int S, int Hq) {
   constexpr int LPR = D / 8;                       // lanes per row
   const int64_t rows = (int64_t)B * S * Hq;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -60,9 +71,6 @@ attn_bwd_pre_kernel(const lt_half* __restrict__ O, const lt_half* __restrict__ d
     const half8 d = as_half8(ld16(dO + off));
 #pragma unroll
     for (int e = 0; e < 8; ++e) s += (float)o[e] * (float)d[e];
-    float4* z = reinterpret_cast<float4*>(dq_acc + row * D + part * 8);
-    z[0] = make_float4(0.f, 0.f, 0.f, 0.f);
-    z[1] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
 #pragma unroll
   for (int m = LPR / 2; m >= 1; m >>= 1) s += __shfl_xor(s, m);
@@ -78,44 +86,31 @@ attn_bwd_pre_kernel(const lt_half* __restrict__ O, const lt_half* __restrict__ d
 }
 
 // ------------------------------------------------------------ kernel 2
-// dS^T [key][query] tile, 128-byte rows.  Byte offset of (key r, query q):
-// the 64-byte half is XORed with bit 1 of r and the 8-byte slot inside it
-// with bits 2..4 of r, so 32 consecutive keys writing one 8-byte query run
-// hit 32 different bank groups, and the transpose reads of 4 consecutive keys
-// land in 4 different 64-byte windows.
-__device__ __forceinline__ int dst_off(int r, int q) {
-  return r * (BQ * 2) + ((q * 2) ^ (((r >> 1) & 1) << 6) ^ (((r >> 2) & 7) << 3));
-}
-
 template <int D>
-struct BwdSmem {
+struct DkdvSmem {
   using RT = RowTile<D, NW>;
-  static constexpr int TILE_Q = BQ * RT::ROWB;
-  static constexpr int DST_PITCH = BQ * 2;          // dS^T row: 64 queries
-  static constexpr int K_OFF = 0;                     // K tile [BKV][D]
-  static constexpr int Q_OFF = K_OFF + BKV * RT::ROWB;          // 2 buffers
-  static constexpr int DO_OFF = Q_OFF + 2 * TILE_Q;             // 2 buffers
-  static constexpr int LSE_OFF = DO_OFF + 2 * TILE_Q;           // 2 x BQ floats
-  static constexpr int DEL_OFF = LSE_OFF + 2 * BQ * 4;          // 2 x BQ floats
-  static constexpr int DST_OFF = DEL_OFF + 2 * BQ * 4;          // dS^T [BKV][BQ]
-  static constexpr int BYTES = DST_OFF + BKV * DST_PITCH;
+  static constexpr int TQ = BQA * RT::ROWB;             // one Q or dO block
+  static constexpr int V_OFF = 0;                        // V tile [BKV][D]
+  static constexpr int Q_OFF = V_OFF + BKV * RT::ROWB;   // 2 buffers
+  static constexpr int DO_OFF = Q_OFF + 2 * TQ;          // 2 buffers
+  // base-2 LSE and D rows: 2 buffers x {LSE2, D} x 256 B (a 4-byte direct
+  // load writes 64 lanes x 4 B; only the first BQA entries are used)
+  static constexpr int ROW_OFF = DO_OFF + 2 * TQ;
+  static constexpr int BYTES = ROW_OFF + 4 * 256;
 };
 
 template <int D>
-__global__ void __launch_bounds__(NW * 64)
-attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
+__global__ void __launch_bounds__(NW * 64, 2)
+attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
                      const lt_half* __restrict__ V, int64_t q_stride, int64_t kv_stride,
                      const lt_half* __restrict__ dO, int64_t o_stride, const float* __restrict__ lse2,
-                     const float* __restrict__ delta, float* __restrict__ dq_acc,
-                     lt_half* __restrict__ dK, lt_half* __restrict__ dV, int64_t dkv_stride, int B,
-                     int S, int Hq, int Hkv, float scale, int causal) {
-  using SM = BwdSmem<D>;
+                     const float* __restrict__ delta, lt_half* __restrict__ dK,
+                     lt_half* __restrict__ dV, int64_t dkv_stride, float* __restrict__ part,
+                     int nsplit, int B, int S, int Hq, int Hkv, float scale, int causal) {
+  using SM = DkdvSmem<D>;
   using RT = RowTile<D, NW>;
   constexpr int KK = D / 16;       // MFMA steps over the head dim
   constexpr int DB = D / 32;       // 32-feature blocks
-  constexpr int QBS = BQ / 32;     // 32-query blocks per tile
-  constexpr int DQ_BLK = DB * QBS / NW;   // dQ output blocks per wave
-  static_assert(DQ_BLK >= 1, "dQ blocks must cover the waves");
   __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
 
   const int tid = threadIdx.x;
@@ -125,10 +120,12 @@ attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
   const int g = lane >> 5;
 
   const int bkv = blockIdx.x % (B * Hkv);
-  const int jt = blockIdx.x / (B * Hkv);          // ascending key tile = descending work
+  const int sp = (blockIdx.x / (B * Hkv)) % nsplit;   // which share of the query heads
+  const int jt = blockIdx.x / (B * Hkv * nsplit);     // ascending key tile = descending work
   const int b = bkv / Hkv;
   const int kvh = bkv % Hkv;
-  const int grp = Hq / Hkv;
+  const int grp = Hq / Hkv / nsplit;                  // query heads of this workgroup
+  const int h0 = kvh * (Hq / Hkv) + sp * grp;         // the first of them
   const int kbase = jt * BKV;
   const int kw0 = kbase + wave * 32;               // this wave's first key
   const int mykey = kw0 + lrow;                    // key owned by this lane (S, dP columns)
@@ -136,21 +133,15 @@ attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
   const lt_half* Kp = K + (int64_t)b * S * kv_stride + (int64_t)kvh * D;
   const lt_half* Vp = V + (int64_t)b * S * kv_stride + (int64_t)kvh * D;
 
-  // ---- K tile -> LDS (B operand of dQ = dS K, read transposed) ----
-  RT::template dma<BKV>(smem + SM::K_OFF, Kp + (int64_t)kbase * kv_stride, kv_stride, S - kbase,
+  // ---- V tile -> LDS (B operand of dP = dO V^T); rows past S read as zero ----
+  RT::template dma<BKV>(smem + SM::V_OFF, Vp + (int64_t)kbase * kv_stride, kv_stride, S - kbase,
                         wave, lane);
-  // ---- K, V fragments (B operands of S = Q K^T and dP = dO V^T) ----
-  half8 kf[KK], vf[KK];
+  // ---- K fragments (B operand of S = Q K^T) ----
+  half8 kf[KK];
 #pragma unroll
-  for (int kk = 0; kk < KK; ++kk) {
-    if (mykey < S) {
-      kf[kk] = as_half8(ld16(Kp + (int64_t)mykey * kv_stride + kk * 16 + g * 8));
-      vf[kk] = as_half8(ld16(Vp + (int64_t)mykey * kv_stride + kk * 16 + g * 8));
-    } else {
-      kf[kk] = as_half8(u32x4{0, 0, 0, 0});
-      vf[kk] = as_half8(u32x4{0, 0, 0, 0});
-    }
-  }
+  for (int kk = 0; kk < KK; ++kk)
+    kf[kk] = mykey < S ? as_half8(ld16(Kp + (int64_t)mykey * kv_stride + kk * 16 + g * 8))
+                       : as_half8(u32x4{0, 0, 0, 0});
 
   f32x16 dkacc[DB], dvacc[DB];
 #pragma unroll
@@ -162,32 +153,31 @@ attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
     }
 
   const float c = scale * kLog2e;
-  const int n_qt = (S + BQ - 1) / BQ;
-  const int qt0 = causal ? kbase / BQ : 0;
-  const int per_head = n_qt - qt0;
+  const int n_qb = (S + BQA - 1) / BQA;
+  const int qb0 = causal ? kbase / BQA : 0;
+  const int per_head = n_qb - qb0;
   const int n_iter = grp * per_head;
 
-  // Query tile `it` = (query head, 64 queries).  Q, dO (rows past S read as
-  // zero) and the base-2 LSE and D rows (zero past S: with zero Q and dO rows
+  // Block `it` = (query head, 32 queries).  Q, dO (rows past S read as zero)
+  // and the base-2 LSE and D entries (zero past S: with zero Q and dO rows
   // those queries contribute nothing) go to LDS by direct loads.
-  auto tile_of = [&](int it, int& h, int& qbase) {
-    h = kvh * grp + it / per_head;
-    qbase = (qt0 + it % per_head) * BQ;
+  auto block_of = [&](int it, int& h, int& qbase) {
+    h = h0 + it / per_head;
+    qbase = (qb0 + it % per_head) * BQA;
   };
   auto stage = [&](int it, int buf) {
     int h, qbase;
-    tile_of(it, h, qbase);
-    RT::template dma<BQ>(smem + SM::Q_OFF + buf * SM::TILE_Q,
-                         Q + ((int64_t)b * S + qbase) * q_stride + (int64_t)h * D, q_stride,
-                         S - qbase, wave, lane);
-    RT::template dma<BQ>(smem + SM::DO_OFF + buf * SM::TILE_Q,
-                         dO + ((int64_t)b * S + qbase) * o_stride + (int64_t)h * D, o_stride,
-                         S - qbase, wave, lane);
+    block_of(it, h, qbase);
+    RT::template dma<BQA>(smem + SM::Q_OFF + buf * SM::TQ,
+                          Q + ((int64_t)b * S + qbase) * q_stride + (int64_t)h * D, q_stride,
+                          S - qbase, wave, lane);
+    RT::template dma<BQA>(smem + SM::DO_OFF + buf * SM::TQ,
+                          dO + ((int64_t)b * S + qbase) * o_stride + (int64_t)h * D, o_stride,
+                          S - qbase, wave, lane);
     if (wave < 2) {
       const float* rowp = (wave == 0 ? lse2 : delta) + ((int64_t)b * Hq + h) * S + qbase;
-      const int nv = S - qbase < BQ ? S - qbase : BQ;
-      lds_dma4_opaque(rowp, (uint32_t)(nv * 4),
-                      smem + (wave == 0 ? SM::LSE_OFF : SM::DEL_OFF) + buf * BQ * 4,
+      const int nv = S - qbase < BQA ? S - qbase : BQA;
+      lds_dma4_opaque(rowp, (uint32_t)(nv * 4), smem + SM::ROW_OFF + buf * 512 + wave * 256,
                       (uint32_t)(lane * 4));
     }
   };
@@ -199,24 +189,20 @@ attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
   for (int it = 0; it < n_iter; ++it) {
     const int cur = it & 1;
     int h, qbase;
-    tile_of(it, h, qbase);
-    const bool more = it + 1 < n_iter;
-    if (more) stage(it + 1, cur ^ 1);
-    const char* qs = smem + SM::Q_OFF + cur * SM::TILE_Q;
-    const char* dos = smem + SM::DO_OFF + cur * SM::TILE_Q;
-    const float* lse_s = reinterpret_cast<const float*>(smem + SM::LSE_OFF + cur * BQ * 4);
-    const float* del_s = reinterpret_cast<const float*>(smem + SM::DEL_OFF + cur * BQ * 4);
+    block_of(it, h, qbase);
+    // that buffer was last read before the previous barrier
+    if (it + 1 < n_iter) stage(it + 1, cur ^ 1);
+    const char* qs = smem + SM::Q_OFF + cur * SM::TQ;
+    const char* dos = smem + SM::DO_OFF + cur * SM::TQ;
+    const float* lse_s = reinterpret_cast<const float*>(smem + SM::ROW_OFF + cur * 512);
+    const float* del_s = reinterpret_cast<const float*>(smem + SM::ROW_OFF + cur * 512 + 256);
 
-    // One 32-query half at a time (keeps the live accumulators small):
-    //   S = Q K^T, dP = dO V^T          (lane owns key `mykey`, 16 query rows)
-    //   P = exp2(s*scale*log2e - LSE2), dS = P (dP - D)
-    //   dS^T -> LDS;  dV^T += dO^T P,  dK^T += Q^T dS
-    // (queries past S have zero Q and dO rows and zero LSE2 and D: finite P,
-    // zero dS and zero contributions)
-    const bool need_mask = (causal && kw0 + 31 > qbase) || kw0 + 32 > S;
-    const int keyl = wave * 32 + lrow;
-#pragma unroll
-    for (int qb = 0; qb < QBS; ++qb) {
+    // causal: all of this wave's keys after all of the block's queries -> P = 0
+    const bool active = (!causal || kw0 <= qbase + BQA - 1) && kw0 < S;
+    if (active) {
+      //   S = Q K^T, dP = dO V^T   (lane owns key `mykey`, 16 query rows)
+      //   P = exp2(s*scale*log2e - LSE2), dS = P (dP - D)
+      //   dV^T += dO^T P,  dK^T += Q^T dS
       f32x16 sacc, pacc;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
@@ -225,14 +211,15 @@ attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
       }
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
-        sacc = mfma32(RT::row_frag(qs, qb * 32, kk, lane), kf[kk], sacc);
-        pacc = mfma32(RT::row_frag(dos, qb * 32, kk, lane), vf[kk], pacc);
+        sacc = mfma32(RT::row_frag(qs, 0, kk, lane), kf[kk], sacc);
+        pacc = mfma32(RT::row_frag(dos, 0, kk, lane),
+                      RT::row_frag(smem + SM::V_OFF, wave * 32, kk, lane), pacc);
       }
 
       float p[16], ds[16];
 #pragma unroll
       for (int rq = 0; rq < 4; ++rq) {
-        const int ql0 = qb * 32 + 8 * rq + 4 * g;
+        const int ql0 = 8 * rq + 4 * g;
         const float4 l4 = *reinterpret_cast<const float4*>(lse_s + ql0);
         const float4 d4 = *reinterpret_cast<const float4*>(del_s + ql0);
         const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
@@ -244,14 +231,13 @@ attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
           ds[r] = pacc[r] - dv[e];
         }
       }
-      if (need_mask) {   // wave-uniform: diagonal or ragged key tile
+      if ((causal && kw0 + 31 > qbase) || kw0 + 32 > S) {   // wave-uniform
         // key > query (causal) or key past S -> P = 0
         const int qlim = causal ? mykey : 0;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int q = qbase + qb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
-          const bool masked = (q < qlim) | (mykey >= S);
-          p[r] = masked ? 0.f : p[r];
+          const int q = qbase + 8 * (r >> 2) + 4 * g + (r & 3);
+          p[r] = ((q < qlim) | (mykey >= S)) ? 0.f : p[r];
         }
       }
 #pragma unroll
@@ -264,77 +250,42 @@ attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
         pds[kc] = pack8(ds[8 * kc], ds[8 * kc + 1], ds[8 * kc + 2], ds[8 * kc + 3],
                         ds[8 * kc + 4], ds[8 * kc + 5], ds[8 * kc + 6], ds[8 * kc + 7]);
       }
-      // dS^T row `keyl`, queries ql0..ql0+3 (8 bytes) for each 4-run
 #pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        const int ql0 = qb * 32 + 8 * rq + 4 * g;
-        const half8& src = pds[rq >> 1];
-        half4 d4h;
+      for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) d4h[e] = src[4 * (rq & 1) + e];
-        *reinterpret_cast<half4*>(smem + SM::DST_OFF + dst_off(keyl, ql0)) = d4h;
-      }
-#pragma unroll
-      for (int db = 0; db < DB; ++db)
-#pragma unroll
-        for (int kc = 0; kc < 2; ++kc) {
-          const int kb = qb * 32 + kc * 16;
-          dvacc[db] = mfma32(RT::template tr_frag<true>(dos, kb, db * 32, lane), pp[kc], dvacc[db]);
-          dkacc[db] = mfma32(RT::template tr_frag<true>(qs, kb, db * 32, lane), pds[kc], dkacc[db]);
+        for (int db = 0; db < DB; ++db) {
+          dvacc[db] = mfma32(RT::template tr_frag<true>(dos, kc * 16, db * 32, lane), pp[kc],
+                             dvacc[db]);
+          dkacc[db] = mfma32(RT::template tr_frag<true>(qs, kc * 16, db * 32, lane), pds[kc],
+                             dkacc[db]);
         }
     }
 
-    __syncthreads();   // dS^T complete
-
-    // ---- dQ (partial over this workgroup's keys) = dS K -> atomics ----
-    // Result lane layout: column d (one per lane), rows q in 4-runs, so each
-    // atomic instruction covers two 128-byte runs of one dQ row.
-#pragma unroll
-    for (int t = 0; t < DQ_BLK; ++t) {
-      const int bi = wave * DQ_BLK + t;
-      const int db = bi / QBS;
-      const int qb = bi % QBS;
-      f32x16 acc;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-#pragma unroll
-      for (int kc = 0; kc < BKV / 16; ++kc) {
-        // dS as A: rows q (qb*32 + lane%32), keys kc*16 + 8*(lane/32) + 0..7,
-        // read transposed from dS^T[key][q]
-        const int q = qb * 32 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-        v4s part[2];
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int key = kc * 16 + 8 * (lane >> 5) + 4 * hh + ((lane & 15) >> 2);
-          part[hh] = lds_read_tr16(smem + SM::DST_OFF + dst_off(key, q));
-        }
-        const half8 sa = as_half8(pack_v4s_pair(part[0], part[1]));
-        const half8 kb = RT::template tr_frag<false>(smem + SM::K_OFF, kc * 16, db * 32, lane);
-        acc = mfma32(sa, kb, acc);
-      }
-      // rows qbase + qb*32 + 0..31 of this head; rows past S are outside the
-      // buffer and their atomics are dropped
-      const int q0 = qbase + qb * 32;
-      const int nv = S - q0 < 32 ? S - q0 : 32;
-      const int rowb = Hq * D * 4;
-      const rsrc_t rs = make_rsrc(dq_acc + (((int64_t)b * S + q0) * Hq + h) * D,
-                                  nv > 0 ? (uint32_t)(nv * rowb) : 0u);
-      const uint32_t lane_off = (uint32_t)((4 * g * Hq * D + db * 32 + lrow) * 4);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const uint32_t off = lane_off + (uint32_t)((8 * (r >> 2) + (r & 3)) * rowb);
-        __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(acc[r], rs, (int)off, 0, 0);
-      }
-    }
-
-    // own direct loads of the next tile are done (only the dQ atomics may
-    // still be in flight), then everyone's are
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(DQ_BLK * 16) : "memory");
+    // next block resident for every wave; nobody reads this buffer any more
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
   }
 
-  // ---- write dK = scale * acc, dV ----
-  if (mykey < S) {
+  // ---- write dK = scale * acc, dV (or this split's FP32 partial sums) ----
+  if (nsplit > 1) {
+    if (mykey < S) {
+      const int64_t rowsz = (int64_t)B * S * Hkv * D;
+      float* pk = part + (int64_t)sp * rowsz + (((int64_t)b * S + mykey) * Hkv + kvh) * D;
+      float* pv = pk + (int64_t)nsplit * rowsz;
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int rq = 0; rq < 4; ++rq) {
+          const int d = db * 32 + 8 * rq + 4 * g;
+          *reinterpret_cast<float4*>(pk + d) =
+              make_float4(dkacc[db][4 * rq], dkacc[db][4 * rq + 1], dkacc[db][4 * rq + 2],
+                          dkacc[db][4 * rq + 3]);
+          *reinterpret_cast<float4*>(pv + d) =
+              make_float4(dvacc[db][4 * rq], dvacc[db][4 * rq + 1], dvacc[db][4 * rq + 2],
+                          dvacc[db][4 * rq + 3]);
+        }
+    }
+  } else if (mykey < S) {
     lt_half* dkp = dK + ((int64_t)b * S + mykey) * dkv_stride + (int64_t)kvh * D;
     lt_half* dvp = dV + ((int64_t)b * S + mykey) * dkv_stride + (int64_t)kvh * D;
 #pragma unroll
@@ -347,31 +298,204 @@ attn_bwd_main_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
           k4[e] = (_Float16)(dkacc[db][4 * rq + e] * scale);
           v4[e] = (_Float16)dvacc[db][4 * rq + e];
         }
-        const int d0 = db * 32 + 8 * rq + 4 * g;
-        *reinterpret_cast<half4*>(dkp + d0) = k4;
-        *reinterpret_cast<half4*>(dvp + d0) = v4;
+        *reinterpret_cast<half4*>(dkp + db * 32 + 8 * rq + 4 * g) = k4;
+        *reinterpret_cast<half4*>(dvp + db * 32 + 8 * rq + 4 * g) = v4;
       }
   }
 }
 
 // ------------------------------------------------------------ kernel 3
 template <int D>
+struct DqSmem {
+  using RT = RowTile<D, NW>;
+  static constexpr int TILE = BKB * RT::ROWB;     // one K or V slice
+  static constexpr int STAGE = 2 * TILE;          // K then V
+};
+
+template <int D>
+__global__ void __launch_bounds__(NW * 64, 2)
+attn_bwd_dq_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
+                   const lt_half* __restrict__ V, int64_t q_stride, int64_t kv_stride,
+                   const lt_half* __restrict__ dO, int64_t o_stride, const float* __restrict__ lse2,
+                   const float* __restrict__ delta, lt_half* __restrict__ dQ, int64_t dq_stride,
+                   int B, int S, int Hq, int Hkv, float scale, int causal) {
+  using SM = DqSmem<D>;
+  using RT = RowTile<D, NW>;
+  constexpr int KB = BKB / 32;     // 32-key blocks per slice
+  constexpr int DB = D / 32;
+  constexpr int KK = D / 16;
+  __shared__ __attribute__((aligned(1024))) char smem[2 * SM::STAGE];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int lrow = lane & 31;
+  const int g = lane >> 5;
+
+  const int n_qt = (S + BQB - 1) / BQB;
+  const int bh = blockIdx.x % (B * Hq);
+  const int qt = causal ? n_qt - 1 - (int)(blockIdx.x / (B * Hq)) : (int)(blockIdx.x / (B * Hq));
+  const int b = bh / Hq;
+  const int h = bh % Hq;
+  const int kvh = h / (Hq / Hkv);
+  const int q0 = qt * BQB;
+  const int qw0 = q0 + wave * 32;
+  const int myq = qw0 + lrow;                      // query owned by this lane
+
+  const lt_half* Kp = K + (int64_t)b * S * kv_stride + (int64_t)kvh * D;
+  const lt_half* Vp = V + (int64_t)b * S * kv_stride + (int64_t)kvh * D;
+  const float c = scale * kLog2e;
+
+  // Q and dO fragments (B operands of S^T = K Q^T and dP^T = V dO^T):
+  // column = this lane's query, reduction indices kk*16 + 8g + 0..7.
+  // Queries past S: zero Q, dO, LSE2 and D give zero dS.
+  half8 qf[KK], of[KK];
+  float l2 = 0.f, dl = 0.f;
+  if (myq < S) {
+    const lt_half* qp = Q + ((int64_t)b * S + myq) * q_stride + (int64_t)h * D + g * 8;
+    const lt_half* op = dO + ((int64_t)b * S + myq) * o_stride + (int64_t)h * D + g * 8;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      qf[kk] = as_half8(ld16(qp + kk * 16));
+      of[kk] = as_half8(ld16(op + kk * 16));
+    }
+    const int64_t ri = ((int64_t)b * Hq + h) * S + myq;
+    l2 = lse2[ri];
+    dl = delta[ri];
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      qf[kk] = as_half8(u32x4{0, 0, 0, 0});
+      of[kk] = as_half8(u32x4{0, 0, 0, 0});
+    }
+  }
+
+  f32x16 dqacc[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dqacc[db][r] = 0.f;
+
+  const int kv_end = causal ? min(S, q0 + BQB) : S;
+  const int n_kv = (kv_end + BKB - 1) / BKB;
+  const int q_hi = min(qw0 + 32, S) - 1;           // last valid query of this wave
+  const int klim = causal ? min(myq + 1, S) : S;   // keys < klim are visible
+
+  // K, V rows past S read as zero (masked below)
+  auto stage_load = [&](int kt, int buf) {
+    char* st = smem + buf * SM::STAGE;
+    const int key0 = kt * BKB;
+    RT::template dma<BKB>(st, Kp + (int64_t)key0 * kv_stride, kv_stride, S - key0, wave, lane);
+    RT::template dma<BKB>(st + SM::TILE, Vp + (int64_t)key0 * kv_stride, kv_stride, S - key0,
+                          wave, lane);
+  };
+  if (n_kv > 0) stage_load(0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+
+  for (int kt = 0; kt < n_kv; ++kt) {
+    const char* ks = smem + (kt & 1) * SM::STAGE;
+    const char* vs = ks + SM::TILE;
+    // that stage was last read before the previous barrier
+    if (kt + 1 < n_kv) stage_load(kt + 1, (kt + 1) & 1);
+
+    const int key0 = kt * BKB;
+    const bool active = (!causal || key0 <= q_hi) && qw0 < S;
+    if (active) {
+      const bool need_mask = (causal && key0 + BKB - 1 > qw0) || key0 + BKB > S;   // wave-uniform
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        //   S^T = K Q^T, dP^T = V dO^T   (lane owns query `myq`, 16 key rows)
+        f32x16 sacc, pacc;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          sacc[r] = 0.f;
+          pacc[r] = 0.f;
+        }
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+          sacc = mfma32(RT::row_frag(ks, kb * 32, kk, lane), qf[kk], sacc);
+          pacc = mfma32(RT::row_frag(vs, kb * 32, kk, lane), of[kk], pacc);
+        }
+        //   dS^T = P^T (dP^T - D),  P^T = exp2(s*scale*log2e - LSE2)
+        float ds[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float p = fast_exp2(fmaf(sacc[r], c, -l2));
+          if (need_mask) {
+            const int key = key0 + kb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+            p = key < klim ? p : 0.f;
+          }
+          ds[r] = p * (pacc[r] - dl);
+        }
+        half8 dsf[2];
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc)
+          dsf[kc] = pack8(ds[8 * kc], ds[8 * kc + 1], ds[8 * kc + 2], ds[8 * kc + 3],
+                          ds[8 * kc + 4], ds[8 * kc + 5], ds[8 * kc + 6], ds[8 * kc + 7]);
+        //   dQ^T += K^T dS^T   (K^T read transposed, keys in accumulator order)
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+          for (int db = 0; db < DB; ++db)
+            dqacc[db] = mfma32(RT::template tr_frag<true>(ks, kb * 32 + kc * 16, db * 32, lane),
+                               dsf[kc], dqacc[db]);
+      }
+    }
+
+    // next slice resident for every wave; nobody reads this stage any more
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+  }
+
+  // ---- dQ = scale * acc -> FP16 ----
+  if (myq < S) {
+    lt_half* qp = dQ + ((int64_t)b * S + myq) * dq_stride + (int64_t)h * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        half4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[e] = (_Float16)(dqacc[db][4 * rq + e] * scale);
+        *reinterpret_cast<half4*>(qp + db * 32 + 8 * rq + 4 * g) = o;
+      }
+  }
+}
+
+// ------------------------------------------------------------ kernel 4
+// Grouped queries split over several dK/dV workgroups: dK = scale * sum of
+// the FP32 partials, dV = sum, in split order (deterministic).  HBM-bound.
+template <int D>
 __global__ void __launch_bounds__(256)
-attn_bwd_dq_kernel(const float* __restrict__ dq_acc, lt_half* __restrict__ dQ, int64_t dq_stride,
-                   int B, int S, int Hq, float scale) {
-  constexpr int LPR = D / 8;
-  const int64_t rows = (int64_t)B * S * Hq;
+attn_bwd_dkdv_sum_kernel(const float* __restrict__ part, int nsplit, lt_half* __restrict__ dK,
+                         lt_half* __restrict__ dV, int64_t dkv_stride, int B, int S, int Hkv,
+                         float scale) {
+  constexpr int CPR = D / 8;                       // 8-element chunks per row
+  const int64_t rowsz = (int64_t)B * S * Hkv * D;
+  const int64_t chunks = (int64_t)B * S * Hkv * CPR;
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t row = gid / LPR;
-  const int part = (int)(gid % LPR);
-  if (row >= rows) return;
-  const int h = (int)(row % Hq);
-  const int64_t bi = row / Hq;
-  const float4* src = reinterpret_cast<const float4*>(dq_acc + row * D + part * 8);
-  const float4 a = src[0], bb = src[1];
-  const half8 o = pack8(a.x * scale, a.y * scale, a.z * scale, a.w * scale, bb.x * scale,
-                        bb.y * scale, bb.z * scale, bb.w * scale);
-  st16(dQ + bi * dq_stride + (int64_t)h * D + part * 8, as_u32x4(o));
+  if (gid >= chunks) return;
+  const int64_t e0 = gid * 8;                      // element offset in [B*S][Hkv][D]
+  const int64_t bs = gid / (Hkv * CPR);
+  const int kvh = (int)((gid / CPR) % Hkv);
+  const int d0 = (int)(gid % CPR) * 8;
+#pragma unroll
+  for (int which = 0; which < 2; ++which) {
+    const float* src = part + (int64_t)which * nsplit * rowsz + e0;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < nsplit; ++t) {
+      const float4 x = *reinterpret_cast<const float4*>(src + (int64_t)t * rowsz);
+      const float4 y = *reinterpret_cast<const float4*>(src + (int64_t)t * rowsz + 4);
+      acc[0] += x.x; acc[1] += x.y; acc[2] += x.z; acc[3] += x.w;
+      acc[4] += y.x; acc[5] += y.y; acc[6] += y.z; acc[7] += y.w;
+    }
+    const float f = which == 0 ? scale : 1.f;
+    const half8 o = pack8(acc[0] * f, acc[1] * f, acc[2] * f, acc[3] * f, acc[4] * f, acc[5] * f,
+                          acc[6] * f, acc[7] * f);
+    lt_half* dst = (which == 0 ? dK : dV) + bs * dkv_stride + (int64_t)kvh * D + d0;
+    st16(dst, as_u32x4(o));
+  }
 }
 
 template <int D>
@@ -381,18 +505,30 @@ hipError_t launch_bwd(const AttnBwdArgs& a, hipStream_t s) {
   const int64_t threads = rows * (D / 8);
   const unsigned eblocks = (unsigned)((threads + 255) / 256);
   hipLaunchKernelGGL((attn_bwd_pre_kernel<D>), dim3(eblocks), dim3(256), 0, s, a.O, a.dO,
-                     a.o_stride, a.LSE, a.delta, a.lse2, a.dq_acc, sh.B, sh.S, sh.Hq);
+                     a.o_stride, a.LSE, a.delta, a.lse2, sh.B, sh.S, sh.Hq);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int n_kt = (sh.S + BKV - 1) / BKV;
-  hipLaunchKernelGGL((attn_bwd_main_kernel<D>), dim3((unsigned)(n_kt * sh.B * sh.Hkv)),
-                     dim3(NW * 64), 0, s, a.Q, a.K, a.V, a.q_stride, a.kv_stride, a.dO, a.o_stride,
-                     a.lse2, a.delta, a.dq_acc, a.dK, a.dV, a.dkv_stride, sh.B, sh.S, sh.Hq, sh.Hkv,
-                     sh.scale, sh.causal);
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D>),
+                     dim3((unsigned)(n_kt * sh.B * sh.Hkv * a.nsplit)), dim3(NW * 64), 0, s, a.Q,
+                     a.K, a.V, a.q_stride, a.kv_stride, a.dO, a.o_stride, a.lse2, a.delta, a.dK,
+                     a.dV, a.dkv_stride, a.part, a.nsplit, sh.B, sh.S, sh.Hq, sh.Hkv, sh.scale,
+                     sh.causal);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((attn_bwd_dq_kernel<D>), dim3(eblocks), dim3(256), 0, s, a.dq_acc, a.dQ,
-                     a.dq_stride, sh.B, sh.S, sh.Hq, sh.scale);
+  if (a.nsplit > 1) {
+    const int64_t chunks = (int64_t)sh.B * sh.S * sh.Hkv * (D / 8);
+    hipLaunchKernelGGL((attn_bwd_dkdv_sum_kernel<D>), dim3((unsigned)((chunks + 255) / 256)),
+                       dim3(256), 0, s, a.part, a.nsplit, a.dK, a.dV, a.dkv_stride, sh.B, sh.S,
+                       sh.Hkv, sh.scale);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const int n_qt = (sh.S + BQB - 1) / BQB;
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<D>), dim3((unsigned)(n_qt * sh.B * sh.Hq)),
+                     dim3(NW * 64), 0, s, a.Q, a.K, a.V, a.q_stride, a.kv_stride, a.dO, a.o_stride,
+                     a.lse2, a.delta, a.dQ, a.dq_stride, sh.B, sh.S, sh.Hq, sh.Hkv, sh.scale,
+                     sh.causal);
   return hipGetLastError();
 }
 

@@ -57,7 +57,8 @@ struct AttnBwdArgs {
   int64_t dq_stride, dkv_stride;
   float* delta;   // workspace: [B, Hq, S]  rowsum(dO * O)
   float* lse2;    // workspace: [B, Hq, S]  LSE * log2(e)
-  float* dq_acc;  // workspace: [B, S, Hq, D]
+  float* part;    // workspace: [2][nsplit][B, S, Hkv, D] partial dK, dV (nsplit > 1 only)
+  int nsplit;     // query-head groups per key tile of the dK/dV pass
 };
 
 // Workspace layout of the attention backward (offsets in bytes).
@@ -66,8 +67,20 @@ inline size_t attn_bwd_delta_bytes(int B, int S, int Hq) {
   return align256((size_t)B * Hq * S * sizeof(float));
 }
 inline size_t attn_bwd_lse2_bytes(int B, int S, int Hq) { return attn_bwd_delta_bytes(B, S, Hq); }
-inline size_t attn_bwd_dq_bytes(int B, int S, int Hq, int D) {
-  return align256((size_t)B * S * Hq * D * sizeof(float));
+// The dK/dV pass runs one workgroup per (128-key tile, batch, kv head, split);
+// with grouped queries and few kv heads the Hq/Hkv query heads of a group are
+// split over the smallest divisor n of Hq/Hkv that gives at least 1024
+// workgroups (all of them if none does), each writing FP32 partial sums.
+inline int attn_bwd_dkdv_splits(int B, int S, int Hq, int Hkv) {
+  const int grp = Hq / Hkv;
+  const int64_t wgs = (int64_t)((S + 127) / 128) * B * Hkv;
+  for (int n = 1; n < grp; ++n)
+    if (grp % n == 0 && wgs * n >= 1024) return n;
+  return grp;
+}
+inline size_t attn_bwd_part_bytes(int B, int S, int Hq, int Hkv, int D) {
+  const int n = attn_bwd_dkdv_splits(B, S, Hq, Hkv);
+  return n > 1 ? align256((size_t)2 * n * B * S * Hkv * D * sizeof(float)) : 0;
 }
 
 hipError_t gemm_f16_launch(const GemmArgs& a, hipStream_t s);

@@ -137,7 +137,7 @@ lt_status lt_attn_fwd(const lt_half* Q, const lt_half* K, const lt_half* V, int6
 size_t lt_attn_bwd_workspace_size(int B, int S, int Hq, int Hkv, int D) {
   if (B < 1 || S < 1 || Hq < 1 || Hkv < 1 || D < 1 || Hq % Hkv) return 0;
   return lt::attn_bwd_delta_bytes(B, S, Hq) + lt::attn_bwd_lse2_bytes(B, S, Hq) +
-         lt::attn_bwd_dq_bytes(B, S, Hq, D);
+         lt::attn_bwd_part_bytes(B, S, Hq, Hkv, D);
 }
 
 lt_status lt_attn_bwd(const lt_half* Q, const lt_half* K, const lt_half* V, int64_t q_row_stride,
@@ -172,7 +172,8 @@ lt_status lt_attn_bwd(const lt_half* Q, const lt_half* K, const lt_half* V, int6
                     reinterpret_cast<float*>(ws),
                     reinterpret_cast<float*>(ws + lt::attn_bwd_delta_bytes(B, S, Hq)),
                     reinterpret_cast<float*>(ws + lt::attn_bwd_delta_bytes(B, S, Hq) +
-                                             lt::attn_bwd_lse2_bytes(B, S, Hq))};
+                                             lt::attn_bwd_lse2_bytes(B, S, Hq)),
+                    lt::attn_bwd_dkdv_splits(B, S, Hq, Hkv)};
   return from_hip(lt::attn_bwd_launch(a, reinterpret_cast<hipStream_t>(stream)), "attn_bwd launch");
 }
 

@@ -94,10 +94,20 @@ def test_attn_fwd_rejects_on_host(kw, status):
     assert _fwd(**kw) == status
 
 
+def _align256(x):
+    return (x + 255) // 256 * 256
+
+
 def test_attn_bwd_workspace():
+    # MHA: D and the base-2 LSE, [B, Hq, S] fp32 each, 256-byte aligned
+    assert lt.lt_attn_bwd_workspace_size(2, 100, 8, 8, 128) == 2 * _align256(4 * 2 * 8 * 100)
+    # GQA with few key tiles: plus fp32 partial dK, dV for every split of the group
+    # (here 4 splits of the 4 query heads per kv head)
     ws = lt.lt_attn_bwd_workspace_size(2, 100, 8, 2, 128)
-    assert ws >= 4 * 2 * 8 * 100 + 4 * 2 * 100 * 8 * 128
+    assert ws == 2 * _align256(4 * 2 * 8 * 100) + _align256(2 * 4 * 2 * 100 * 2 * 128 * 4)
     assert ws % 256 == 0
+    # enough kv heads x key tiles (1024 workgroups): no split, no partials
+    assert lt.lt_attn_bwd_workspace_size(1, 4096, 128, 32, 128) == 2 * _align256(4 * 128 * 4096)
     assert lt.lt_attn_bwd_workspace_size(0, 100, 8, 2, 128) == 0
     assert lt.lt_attn_bwd_workspace_size(1, 100, 8, 3, 128) == 0
     args = [FAKE, FAKE, FAKE, 1536, 1536, FAKE, FAKE, 1024, FAKE, FAKE, FAKE, FAKE, 1536, 1536]

@@ -166,6 +166,9 @@ def test_attention_causality_and_invariants(env):
 @pytest.mark.parametrize("name,B,S,Hq,Hkv,D,heads", [
     ("llama2-7b", 1, 4096, 32, 32, 128, [(0, 0), (0, 31)]),
     ("qwen2.5-32b", 1, 4096, 40, 8, 128, [(0, 5)]),
+    # 2 x 8 kv heads x 32 key tiles: the group's 8 query heads split in two
+    # dK/dV workgroups per key tile, partial sums added by the sum kernel
+    ("llama2-70b", 2, 4096, 64, 8, 128, [(1, 3)]),
 ])
 def test_attention_full_size_sampled(env, name, B, S, Hq, Hkv, D, heads):
     """Full-size attention in the benchmark's launch configuration; whole
