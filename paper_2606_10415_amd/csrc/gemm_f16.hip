@@ -26,6 +26,8 @@
 //     grouped eight tile-rows at a time for L2 reuse of A and B.
 //   Buffer loads return zeros out of range, which provides the M, N and K
 //   tails without branches.
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -39,7 +41,9 @@ namespace {
 //       different bank groups.
 //   !KC (row index contiguous in HBM): LDS k-major, 2R bytes per k-row;
 //       16-byte chunk c (rows 8c..8c+7) of k-row k sits at position
-//       ((c >> 2) ^ (k & 3)) * 4 + (c & 3).
+//       kpos(c, k) = ((c >> 2) ^ (k & 3)) * 4 + ((c & 3) ^ 2 * ((k >> 3) & 1)):
+//       the transpose reads of one MFMA operand (4 k-rows x 32 bytes per
+//       16-lane group, groups 8 k-rows apart) then hit every bank once.
 // Both are filled by direct global -> LDS loads issued as opaque
 // instructions, so the caller orders them with explicit vmcnt waits.
 template <int R, int BK, bool KC, int NT>
@@ -55,6 +59,10 @@ struct Operand {
   static_assert(CPR >= 4 && CPR <= 16, "KC layout needs 32 <= BK <= 128");
 
   __device__ static __forceinline__ int swz(int r) { return (r / (16 / CPR)) & (CPR - 1); }
+  // !KC chunk position; an involution in c for fixed k
+  __device__ static __forceinline__ int kpos(int c, int k) {
+    return (((c >> 2) ^ (k & 3)) << 2) | ((c & 3) ^ (((k >> 3) & 1) << 1));
+  }
 
   uint32_t voff[PERW];
   const lt_half* base;
@@ -81,8 +89,7 @@ struct Operand {
 #pragma unroll
       for (int t = 0; t < PERW; ++t) {
         const int k = (wave * PERW + t) * KR_PER + lane / LPR;
-        const int p = lane % LPR;
-        const int c = (((p >> 2) ^ (k & 3)) << 2) | (p & 3);
+        const int c = kpos(lane % LPR, k);             // chunk that lands at position lane % LPR
         voff[t] = row0 + c * 8 < rows ? (uint32_t)((k * ld + c * 8) * 2) : kOOB;
       }
     }
@@ -118,26 +125,26 @@ struct Operand {
     }
   }
 
-  // MFMA operand: rows rb..rb+31 (lane row = lane % 32), reduction indices
-  // kk*16 + 8*(lane/32) + 0..7.
+  // MFMA operand (16x16x32): rows rb..rb+15 (lane row = lane % 16),
+  // reduction indices kk*32 + 8*(lane/16) + 0..7.
   __device__ __forceinline__ half8 frag(const char* lds, int rb, int kk, int lane) const {
     if constexpr (KC) {
-      const int r = rb + (lane & 31);
-      const int c = kk * 2 + (lane >> 5);
+      const int r = rb + (lane & 15);
+      const int c = kk * 4 + (lane >> 4);
       return as_half8(*reinterpret_cast<const u32x4*>(lds + r * (CPR * 16) + ((c ^ swz(r)) << 4)));
     } else {
-      // Two transpose reads (h = 0, 1).  Lane L reads 4 rows at
-      // m = rb + 16*((L/16)%2) + 4*(L%4) of k-row kk*16 + 8*(L/32) + 4h + (L%16)/4,
-      // and receives rows rb + L%32 of k-rows kk*16 + 8*(L/32) + 4h + 0..3.
-      const int m = rb + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+      // Two transpose reads (h = 0, 1).  Within 16-lane group G = L/16, lane
+      // s = L%16 reads the 4 rows at m = rb + 4*(s%4) of k-row
+      // kk*32 + 8G + 4h + s/4, and receives row rb + s of k-rows
+      // kk*32 + 8G + 4h + 0..3.
+      const int m = rb + 4 * (lane & 3);
       const int c = m >> 3;
       const int inoff = (m & 7) * 2;
       v4s part[2];
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
-        const int k = kk * 16 + 8 * (lane >> 5) + 4 * h + ((lane & 15) >> 2);
-        const int pc = (((c >> 2) ^ (k & 3)) << 2) | (c & 3);
-        part[h] = lds_read_tr16(lds + k * (2 * R) + pc * 16 + inoff);
+        const int k = kk * 32 + 8 * (lane >> 4) + 4 * h + ((lane & 15) >> 2);
+        part[h] = lds_read_tr16(lds + k * (2 * R) + kpos(c, k) * 16 + inoff);
       }
       return as_half8(pack_v4s_pair(part[0], part[1]));
     }
@@ -168,7 +175,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
                 int tiles_n) {
   constexpr int NT = WGM * WGN * kWave;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;   // wave tile
-  constexpr int TM = WTM / 32, TN = WTN / 32;     // 32x32 MFMA blocks per wave
+  constexpr int TM = WTM / 16, TN = WTN / 16;     // 16x16 MFMA blocks per wave
   using OA = Operand<BM, BK, !TA, NT>;
   using OB = Operand<BN, BK, TB, NT>;
   constexpr int STAGE = OA::BYTES + OB::BYTES;
@@ -202,13 +209,13 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   oa.init(A, lda, m0, M, wave, lane);
   ob.init(B, ldb, n0, N, wave, lane);
 
-  f32x16 acc[TM][TN];
+  f32x4 acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+      for (int r = 0; r < 4; ++r) acc[i][j][r] = 0.f;
 
   const int nk = (int)((K + BK - 1) / BK);
   auto kvalid = [&](int kt) {
@@ -221,13 +228,9 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
     oa.load(st, (int64_t)kt * BK, kvalid(kt), wave, lane);
     ob.load(st + OA::BYTES, (int64_t)kt * BK, kvalid(kt), wave, lane);
   };
-  half8 fa[2][TM], fb[2][TN];
-  auto frag_load = [&](const char* st, int kk, int s) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i) fa[s][i] = oa.frag(st, wm * WTM + i * 32, kk, lane);
-#pragma unroll
-    for (int j = 0; j < TN; ++j) fb[s][j] = ob.frag(st + OA::BYTES, wn * WTN + j * 32, kk, lane);
-  };
+  // Fragments: A in place (each re-read right after its last use), B
+  // double-buffered (used by every A row of a step).
+  half8 fa[TM], fb[2][TN];
 
   // ---- prologue: slices 0 .. NS-2 in flight, wait for slice 0 ----
 #pragma unroll
@@ -235,80 +238,93 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
     if (s < nk) issue(s);
   wait_slices<PER_SLICE, NS - 2>(min(NS - 2, nk - 1));
   __syncthreads();
-  if (nk > 0) frag_load(smem, 0, 0);
+  if (nk > 0) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) fa[i] = oa.frag(smem, wm * WTM + i * 16, 0, lane);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) fb[0][j] = ob.frag(smem + OA::BYTES, wn * WTN + j * 16, 0, lane);
+  }
+
+  // One MFMA step on (fa, fb[S]).  With LD, the fragments of the next step
+  // (32-wide k-step kk of stage st) are read meanwhile: after the MFMAs of A
+  // row i come the reads of fa[i] and, for the first TN rows, of fb[S^1][i],
+  // so every read overlaps the MFMAs that follow it.  S and LD are
+  // compile-time constants so that the fragment arrays stay in registers.
+  constexpr int KS = BK / 32;
+  static_assert(KS % 2 == 0, "B fragments alternate buffers within a slice");
+  constexpr int RA = TA ? 2 : 1;   // LDS reads per A fragment (transpose reads: 2)
+  constexpr int RB = TB ? 1 : 2;   // ... per B fragment
+  auto step = [&](auto S_, auto LD_, const char* st, int kk) {
+    constexpr int S = decltype(S_)::value;
+    constexpr bool LD = decltype(LD_)::value;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = mfma16(fb[S][j], fa[i], acc[i][j]);
+      if constexpr (LD) {
+        if (i < TN) fb[S ^ 1][i] = ob.frag(st + OA::BYTES, wn * WTN + i * 16, kk, lane);
+        fa[i] = oa.frag(st, wm * WTM + i * 16, kk, lane);
+      }
+    }
+    if constexpr (LD) {
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, TN, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, RB + RA, 0);
+      }
+#pragma unroll
+      for (int i = TN; i < TM; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, TN, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, RA, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  using C0 = std::integral_constant<int, 0>;
+  using C1 = std::integral_constant<int, 1>;
+  using YES = std::integral_constant<bool, true>;
 
   // Per slice kt: the loads of slice kt+NS-1 go out first (into the stage
-  // that slice kt-1 used); MFMA step kk runs on fragments read during step
-  // kk-1.  The barrier sits before the last step, whose fragments are already
-  // in registers, so that the first fragments of slice kt+1 are read while
-  // that step's MFMAs execute.
-  constexpr int KS = BK / 16;
-  auto mfma_step = [&](int s) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(fb[s][j], fa[s][i], acc[i][j]);
-  };
-  auto interleave = [&]() {
-    // pair this step's MFMAs with the next step's LDS reads
-    constexpr int NRD = (TA ? 2 : 1) * TM + (TB ? 1 : 2) * TN;
-    constexpr int NMF = TM * TN;
-    constexpr int NPAIR = NRD < NMF ? NRD : NMF;
-#pragma unroll
-    for (int t = 0; t < NPAIR; ++t) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    if (NMF > NPAIR) __builtin_amdgcn_sched_group_barrier(0x008, NMF - NPAIR, 0);
-    __builtin_amdgcn_sched_barrier(0);
-  };
-
+  // that slice kt-1 used).  The barrier sits before the last step, whose
+  // fragments are already in registers, so that the first fragments of
+  // slice kt+1 are read while that step's MFMAs execute.
   for (int kt = 0; kt < nk; ++kt) {
     const char* cur = stage_of(kt);
     // its stage was last read before the previous iteration's barrier
     if (kt + NS - 1 < nk) issue(kt + NS - 1);
-#pragma unroll
-    for (int kk = 0; kk < KS - 1; ++kk) {
-      frag_load(cur, kk + 1, (kk + 1) & 1);
-      mfma_step(kk & 1);
-      interleave();
-    }
+    static_assert(KS == 2, "one step before and one after the slice barrier");
+    step(C0{}, YES{}, cur, 1);
     // slice kt+1 resident for all waves (later slices may stay in flight);
     // nobody reads `cur` after this point
     wait_slices<PER_SLICE, NS - 2>(min(kt + NS - 1, nk - 1) - (kt + 1));
     __syncthreads();
-    const bool more = kt + 1 < nk;
-    if (more) frag_load(stage_of(kt + 1), 0, 0);
-    mfma_step((KS - 1) & 1);
-    if (more) interleave();
+    // (after the last slice these reads of a stale stage are unused; reading
+    // unconditionally keeps one copy of the fragments live across the loop)
+    step(C1{}, YES{}, stage_of(kt + 1), 0);
   }
 
   // ---- epilogue: C[m][n..n+3] = alpha * acc + beta * R[m][n..n+3] ----
-  const int lrow = lane & 31;
-  const int lhalf = lane >> 5;
+  // lane holds column m = ... + lane % 16 and rows n = ... + 4*(lane/16) + 0..3
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
-    const int64_t m = m0 + wm * WTM + i * 32 + lrow;
+    const int64_t m = m0 + wm * WTM + i * 16 + (lane & 15);
     if (m >= M) continue;
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
+      const int64_t n = n0 + wn * WTN + j * 16 + 4 * (lane >> 4);
+      if (n >= N) continue;
+      float v[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int64_t n = n0 + wn * WTN + j * 32 + q * 8 + lhalf * 4;
-        if (n >= N) continue;
-        float v[4];
+      for (int e = 0; e < 4; ++e) v[e] = alpha * acc[i][j][e];
+      if (beta != 0.f) {
+        const half4 c = *reinterpret_cast<const half4*>(R + m * ldr + n);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = alpha * acc[i][j][4 * q + e];
-        if (beta != 0.f) {
-          const half4 c = *reinterpret_cast<const half4*>(R + m * ldr + n);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] += beta * (float)c[e];
-        }
-        half4 o;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) o[e] = (_Float16)v[e];
-        *reinterpret_cast<half4*>(C + m * ldc + n) = o;
+        for (int e = 0; e < 4; ++e) v[e] += beta * (float)c[e];
       }
+      half4 o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) o[e] = (_Float16)v[e];
+      *reinterpret_cast<half4*>(C + m * ldc + n) = o;
     }
   }
 }
