@@ -172,7 +172,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
                 const lt_half* __restrict__ A, int64_t lda,
                 const lt_half* __restrict__ B, int64_t ldb, float beta,
                 const lt_half* R, int64_t ldr, lt_half* C, int64_t ldc, int tiles_m,
-                int tiles_n) {
+                int tiles_n, int group_m) {
   constexpr int NT = WGM * WGN * kWave;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;   // wave tile
   constexpr int TM = WTM / 16, TN = WTN / 16;     // 16x16 MFMA blocks per wave
@@ -189,17 +189,18 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   const int wm = wave / WGN;
   const int wn = wave % WGN;
 
-  // ---- tile ordering: contiguous range per XCD, then grouped along M ----
+  // ---- tile ordering: contiguous range per XCD (consecutive workgroups go
+  // to the 8 XCDs in turn), then column-major within groups of group_m
+  // tile rows, so that the tiles resident on one XCD share A and B panels ----
   int pid = blockIdx.x;
   const int nwg = gridDim.x;
   if ((nwg & 7) == 0) {
     const int per = nwg >> 3;
     pid = (pid & 7) * per + (pid >> 3);
   }
-  constexpr int GROUP_M = 8;
-  const int group_size = GROUP_M * tiles_n;
-  const int first_m = (pid / group_size) * GROUP_M;
-  const int gm = min(tiles_m - first_m, GROUP_M);
+  const int group_size = group_m * tiles_n;
+  const int first_m = (pid / group_size) * group_m;
+  const int gm = min(tiles_m - first_m, group_m);
   const int in_group = pid % group_size;
   const int64_t m0 = (int64_t)(first_m + in_group % gm) * BM;
   const int64_t n0 = (int64_t)(in_group / gm) * BN;
@@ -254,6 +255,11 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   static_assert(KS % 2 == 0, "B fragments alternate buffers within a slice");
   constexpr int RA = TA ? 2 : 1;   // LDS reads per A fragment (transpose reads: 2)
   constexpr int RB = TB ? 1 : 2;   // ... per B fragment
+  // B fragments read after A row i: fb[j] for j % TM == i (BPI of them while
+  // i < NBI; one for each of the first TN rows when TN <= TM).
+  static_assert(TN <= TM || TN % TM == 0, "B fragments must spread over the A rows");
+  constexpr int BPI = TN <= TM ? 1 : TN / TM;
+  constexpr int NBI = TN <= TM ? TN : TM;
   auto step = [&](auto S_, auto LD_, const char* st, int kk) {
     constexpr int S = decltype(S_)::value;
     constexpr bool LD = decltype(LD_)::value;
@@ -262,18 +268,24 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
 #pragma unroll
       for (int j = 0; j < TN; ++j) acc[i][j] = mfma16(fb[S][j], fa[i], acc[i][j]);
       if constexpr (LD) {
-        if (i < TN) fb[S ^ 1][i] = ob.frag(st + OA::BYTES, wn * WTN + i * 16, kk, lane);
+        if (i < NBI) {
+#pragma unroll
+          for (int q = 0; q < BPI; ++q) {
+            const int j = i + q * TM;
+            fb[S ^ 1][j] = ob.frag(st + OA::BYTES, wn * WTN + j * 16, kk, lane);
+          }
+        }
         fa[i] = oa.frag(st, wm * WTM + i * 16, kk, lane);
       }
     }
     if constexpr (LD) {
 #pragma unroll
-      for (int i = 0; i < TN; ++i) {
+      for (int i = 0; i < NBI; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, TN, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, RB + RA, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, BPI * RB + RA, 0);
       }
 #pragma unroll
-      for (int i = TN; i < TM; ++i) {
+      for (int i = NBI; i < TM; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, TN, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, RA, 0);
       }
@@ -335,7 +347,7 @@ hipError_t launch(const GemmArgs& g, hipStream_t s) {
   const int tiles_n = (int)((g.N + BN - 1) / BN);
   hipLaunchKernelGGL((gemm_f16_kernel<BM, BN, WGM, WGN, BK, NS, TA, TB>), dim3(tiles_m * tiles_n),
                      dim3(WGM * WGN * kWave), 0, s, g.M, g.N, g.K, g.alpha, g.A, g.lda, g.B, g.ldb,
-                     g.beta, g.R, g.ldr, g.C, g.ldc, tiles_m, tiles_n);
+                     g.beta, g.R, g.ldr, g.C, g.ldc, tiles_m, tiles_n, 8);
   return hipGetLastError();
 }
 

@@ -1,7 +1,7 @@
 """GPU parity of lt_attn_fwd / lt_attn_bwd against the float64 oracle.
 
 Bars (written here, derived in the design doc):
-  O: relative Frobenius error <= 5e-3;  LSE: max abs error <= 2e-3;
+  O: relative Frobenius error <= 5e-3;  LSE: max abs error <= 1e-4;
   dQ, dK, dV: relative Frobenius error <= 1e-2.
 Also checked on the GPU outputs: causality (future keys / values do not
 change O or dQ of earlier rows: bit-identical), sum_j dK_j ~ 0 and
@@ -21,6 +21,10 @@ from paper_2606_10415_amd.synth import attention_inputs
 from conftest import rel_f
 
 pytestmark = pytest.mark.gpu
+
+# |LSE| reaches ~200 in the large-score case, where one fp32 ulp is 1.5e-5:
+# 1e-4 allows the ~2 ulps of the fp32 score sums, exp2/log and row sum.
+LSE_ABS_TOL = 1e-4
 
 
 @pytest.fixture(scope="module")
@@ -83,28 +87,38 @@ def check_against_oracle(x, got, causal=True, heads=None, kv_heads=None):
     D = q.shape[3]
     scale = 1.0 / math.sqrt(D)
     o_ref, lse_ref = oracle.attn_fwd(q, k, v, scale, causal, heads=heads)
-    if heads is None:
-        assert rel_f(got["O"], o_ref) <= 5e-3
-        assert np.max(np.abs(got["LSE"] - lse_ref)) <= 2e-3
-    else:
-        for b, h in heads:
-            assert rel_f(got["O"][b, :, h], o_ref[b, :, h]) <= 5e-3
-            assert np.max(np.abs(got["LSE"][b, h] - lse_ref[b, h])) <= 2e-3
-    if "dQ" not in got:
-        return
-    # per-op parity: the oracle backward gets the same fp16 inputs (its own P and row term)
-    dq, dk, dv, _ = oracle.attn_bwd(q, k, v, do, scale, causal, kv_heads=kv_heads)
-    if kv_heads is None:
-        assert rel_f(got["dQ"], dq) <= 1e-2
-        assert rel_f(got["dK"], dk) <= 1e-2
-        assert rel_f(got["dV"], dv) <= 1e-2
-    else:
+    sel = [(slice(None), slice(None))] if heads is None else [(b, h) for b, h in heads]
+    err = {"O": 0.0, "LSE": 0.0}
+    for b, h in sel:
+        o_g = got["O"][b, :, h] if heads is not None else got["O"]
+        o_r = o_ref[b, :, h] if heads is not None else o_ref
+        l_g = got["LSE"][b, h] if heads is not None else got["LSE"]
+        l_r = lse_ref[b, h] if heads is not None else lse_ref
+        err["O"] = max(err["O"], rel_f(o_g, o_r))
+        err["LSE"] = max(err["LSE"], float(np.max(np.abs(l_g - l_r))))
+    if "dQ" in got:
+        # per-op parity: the oracle backward gets the same fp16 inputs (its own P and row term)
+        dq, dk, dv, _ = oracle.attn_bwd(q, k, v, do, scale, causal, kv_heads=kv_heads)
         g = q.shape[2] // k.shape[2]
-        for b, kv in kv_heads:
-            hs = slice(kv * g, kv * g + g)
-            assert rel_f(got["dQ"][b, :, hs], dq[b, :, hs]) <= 1e-2
-            assert rel_f(got["dK"][b, :, kv], dk[b, :, kv]) <= 1e-2
-            assert rel_f(got["dV"][b, :, kv], dv[b, :, kv]) <= 1e-2
+        kv_sel = [(slice(None), slice(None), slice(None))] if kv_heads is None else \
+            [(b, slice(kv * g, kv * g + g), kv) for b, kv in kv_heads]
+        for name in ("dQ", "dK", "dV"):
+            err[name] = 0.0
+        for b, hs, kv in kv_sel:
+            if kv_heads is None:
+                pairs = [("dQ", got["dQ"], dq), ("dK", got["dK"], dk), ("dV", got["dV"], dv)]
+            else:
+                pairs = [("dQ", got["dQ"][b, :, hs], dq[b, :, hs]),
+                         ("dK", got["dK"][b, :, kv], dk[b, :, kv]),
+                         ("dV", got["dV"][b, :, kv], dv[b, :, kv])]
+            for name, a_, r_ in pairs:
+                err[name] = max(err[name], rel_f(a_, r_))
+    print("  errors: " + ", ".join(f"{k_} {v_:.3e}" for k_, v_ in err.items()), flush=True)
+    assert err["O"] <= 5e-3
+    assert err["LSE"] <= LSE_ABS_TOL
+    for name in ("dQ", "dK", "dV"):
+        if name in err:
+            assert err[name] <= 1e-2, name
 
 
 CASES = [
