@@ -180,7 +180,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   using OB = Operand<BN, BK, TB, NT>;
   constexpr int STAGE = OA::BYTES + OB::BYTES;
   constexpr int PER_SLICE = OA::PERW + OB::PERW;  // direct loads per wave per slice
-  static_assert(NS >= 2 && (NS - 2) * PER_SLICE <= 63, "vmcnt range");
+  static_assert(NS >= 2 && (NS - 1) * PER_SLICE <= 63, "vmcnt range");
   __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
 
   const int tid = threadIdx.x;
@@ -233,11 +233,11 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   // double-buffered (used by every A row of a step).
   half8 fa[TM], fb[2][TN];
 
-  // ---- prologue: slices 0 .. NS-2 in flight, wait for slice 0 ----
+  // ---- prologue: slices 0 .. NS-1 in flight, wait for slice 0 ----
 #pragma unroll
-  for (int s = 0; s < NS - 1; ++s)
+  for (int s = 0; s < NS; ++s)
     if (s < nk) issue(s);
-  wait_slices<PER_SLICE, NS - 2>(min(NS - 2, nk - 1));
+  wait_slices<PER_SLICE, NS - 1>(min(NS - 1, nk - 1));
   __syncthreads();
   if (nk > 0) {
 #pragma unroll
@@ -260,13 +260,14 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   static_assert(TN <= TM || TN % TM == 0, "B fragments must spread over the A rows");
   constexpr int BPI = TN <= TM ? 1 : TN / TM;
   constexpr int NBI = TN <= TM ? TN : TM;
-  auto step = [&](auto S_, auto LD_, const char* st, int kk) {
+  auto step = [&](auto S_, auto LD_, const char* st, int kk, auto&& after_first_row) {
     constexpr int S = decltype(S_)::value;
     constexpr bool LD = decltype(LD_)::value;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
       for (int j = 0; j < TN; ++j) acc[i][j] = mfma16(fb[S][j], fa[i], acc[i][j]);
+      if (i == 0) after_first_row();
       if constexpr (LD) {
         if (i < NBI) {
 #pragma unroll
@@ -296,23 +297,22 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   using C1 = std::integral_constant<int, 1>;
   using YES = std::integral_constant<bool, true>;
 
-  // Per slice kt: the loads of slice kt+NS-1 go out first (into the stage
-  // that slice kt-1 used).  The barrier sits before the last step, whose
-  // fragments are already in registers, so that the first fragments of
-  // slice kt+1 are read while that step's MFMAs execute.
+  // Per slice kt: step 0, then the barrier after which slice kt+1 is
+  // resident and nobody reads slice kt's stage any more.  Step 1 runs on
+  // registers while reading slice kt+1's first fragments; after its first
+  // MFMAs are queued, the loads of slice kt+NS go into the freed stage,
+  // almost a full slice ahead of their wait.
   for (int kt = 0; kt < nk; ++kt) {
-    const char* cur = stage_of(kt);
-    // its stage was last read before the previous iteration's barrier
-    if (kt + NS - 1 < nk) issue(kt + NS - 1);
     static_assert(KS == 2, "one step before and one after the slice barrier");
-    step(C0{}, YES{}, cur, 1);
-    // slice kt+1 resident for all waves (later slices may stay in flight);
-    // nobody reads `cur` after this point
+    step(C0{}, YES{}, stage_of(kt), 1, [] {});
+    // slices after kt+1 that are already issued may stay in flight
     wait_slices<PER_SLICE, NS - 2>(min(kt + NS - 1, nk - 1) - (kt + 1));
     __syncthreads();
     // (after the last slice these reads of a stale stage are unused; reading
     // unconditionally keeps one copy of the fragments live across the loop)
-    step(C1{}, YES{}, stage_of(kt + 1), 0);
+    step(C1{}, YES{}, stage_of(kt + 1), 0, [&] {
+      if (kt + NS < nk) issue(kt + NS);
+    });
   }
 
   // ---- epilogue: C[m][n..n+3] = alpha * acc + beta * R[m][n..n+3] ----
