@@ -39,9 +39,9 @@ PEAK_HBM_GBS = 8000.0
 # them makes bench report traffic as null until the counters are taken again.
 GEMM_TRAFFIC = {
     "workload": "llama2-7b",
-    "sources_sha256": "dcf1211fae4fc600dde8ec2bf0ae5a50069d2c8c0b3f66d321de9d2433ebe563",
-    "fetch_bytes_per_launch": 691088867,
-    "write_bytes_per_launch": 88791967,
+    "sources_sha256": "158f3efbd186e8244d7a7019521c88829ae191a71dd8c31e89aa64a6886fc7cb",
+    "fetch_bytes_per_launch": 668611271,
+    "write_bytes_per_launch": 81576661,
 }
 GEMM_SOURCES = ("paper_2606_10415_amd/csrc/gemm_f16.hip", "paper_2606_10415_amd/csrc/common.hpp")
 
