@@ -10,11 +10,11 @@
 // Three kernels (four with grouped queries), none with an atomic:
 //   1. attn_bwd_pre : D_i = rowsum(dO_i * O_i) (one 8/16-lane group per row,
 //                     shuffle reduction) and the LSE in base 2.  HBM-bound.
-//   2. attn_bwd_dkdv: key-major.  One workgroup per (batch, kv head, 128-key
-//                     tile); each of the 4 waves owns 32 keys and keeps their
+//   2. attn_bwd_dkdv: key-major.  One workgroup per (batch, kv head, 256-key
+//                     tile); each of the 8 waves owns 32 keys and keeps their
 //                     K fragments and the dK, dV accumulators in registers for
 //                     the whole loop over the GQA group's query heads and the
-//                     causal 32-query blocks (the paper's GSM reduction of
+//                     causal 64-query blocks (the paper's GSM reduction of
 //                     GV / GK becomes register accumulation, and the GQA sum
 //                     is the same loop).  V stays in LDS; Q, dO, LSE and D
 //                     blocks stream HBM -> LDS by direct loads, double-buffered.
@@ -44,9 +44,10 @@
 namespace lt {
 namespace {
 
-constexpr int NW = 4;          // waves per workgroup
-constexpr int BKV = 128;       // dK/dV: keys per workgroup (32 per wave)
-constexpr int BQA = 32;        // dK/dV: queries per block
+constexpr int NWA = 8;         // dK/dV: waves per workgroup
+constexpr int BKV = NWA * 32;  // dK/dV: keys per workgroup (32 per wave)
+constexpr int BQA = 64;        // dK/dV: queries per block (two 32-query halves)
+constexpr int NW = 4;          // dQ: waves per workgroup
 constexpr int BQB = NW * 32;   // dQ: queries per workgroup (32 per wave)
 constexpr int BKB = 64;        // dQ: keys per slice
 constexpr float kLog2e = 1.4426950408889634f;
@@ -88,19 +89,20 @@ attn_bwd_pre_kernel(const lt_half* __restrict__ O, const lt_half* __restrict__ d
 // ------------------------------------------------------------ kernel 2
 template <int D>
 struct DkdvSmem {
-  using RT = RowTile<D, NW>;
+  using RT = RowTile<D, NWA>;
   static constexpr int TQ = BQA * RT::ROWB;             // one Q or dO block
   static constexpr int V_OFF = 0;                        // V tile [BKV][D]
   static constexpr int Q_OFF = V_OFF + BKV * RT::ROWB;   // 2 buffers
   static constexpr int DO_OFF = Q_OFF + 2 * TQ;          // 2 buffers
-  // base-2 LSE and D rows: 2 buffers x {LSE2, D} x 256 B (a 4-byte direct
-  // load writes 64 lanes x 4 B; only the first BQA entries are used)
+  // base-2 LSE and D rows: 2 buffers x {LSE2, D} x 256 B (one 4-byte direct
+  // load of 64 lanes each)
+  static_assert(BQA == 64, "one 4-byte direct load per row vector");
   static constexpr int ROW_OFF = DO_OFF + 2 * TQ;
   static constexpr int BYTES = ROW_OFF + 4 * 256;
 };
 
 template <int D>
-__global__ void __launch_bounds__(NW * 64, 2)
+__global__ void __launch_bounds__(NWA * 64, 1)
 attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
                      const lt_half* __restrict__ V, int64_t q_stride, int64_t kv_stride,
                      const lt_half* __restrict__ dO, int64_t o_stride, const float* __restrict__ lse2,
@@ -108,7 +110,7 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
                      lt_half* __restrict__ dV, int64_t dkv_stride, float* __restrict__ part,
                      int nsplit, int B, int S, int Hq, int Hkv, float scale, int causal) {
   using SM = DkdvSmem<D>;
-  using RT = RowTile<D, NW>;
+  using RT = RowTile<D, NWA>;
   constexpr int KK = D / 16;       // MFMA steps over the head dim
   constexpr int DB = D / 32;       // 32-feature blocks
   __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
@@ -197,8 +199,12 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
     const float* lse_s = reinterpret_cast<const float*>(smem + SM::ROW_OFF + cur * 512);
     const float* del_s = reinterpret_cast<const float*>(smem + SM::ROW_OFF + cur * 512 + 256);
 
-    // causal: all of this wave's keys after all of the block's queries -> P = 0
-    const bool active = (!causal || kw0 <= qbase + BQA - 1) && kw0 < S;
+#pragma nounroll
+    for (int hq = 0; hq < BQA / 32; ++hq) {
+    // 32-query half hq of the block; causal: all of this wave's keys after
+    // all of its queries -> P = 0
+    const int qh = qbase + hq * 32;
+    const bool active = (!causal || kw0 <= qh + 31) && kw0 < S;
     if (active) {
       //   S = Q K^T, dP = dO V^T   (lane owns key `mykey`, 16 query rows)
       //   P = exp2(s*scale*log2e - LSE2), dS = P (dP - D)
@@ -211,15 +217,15 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
       }
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
-        sacc = mfma32(RT::row_frag(qs, 0, kk, lane), kf[kk], sacc);
-        pacc = mfma32(RT::row_frag(dos, 0, kk, lane),
+        sacc = mfma32(RT::row_frag(qs, hq * 32, kk, lane), kf[kk], sacc);
+        pacc = mfma32(RT::row_frag(dos, hq * 32, kk, lane),
                       RT::row_frag(smem + SM::V_OFF, wave * 32, kk, lane), pacc);
       }
 
       float p[16], ds[16];
 #pragma unroll
       for (int rq = 0; rq < 4; ++rq) {
-        const int ql0 = 8 * rq + 4 * g;
+        const int ql0 = hq * 32 + 8 * rq + 4 * g;
         const float4 l4 = *reinterpret_cast<const float4*>(lse_s + ql0);
         const float4 d4 = *reinterpret_cast<const float4*>(del_s + ql0);
         const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
@@ -231,12 +237,12 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
           ds[r] = pacc[r] - dv[e];
         }
       }
-      if ((causal && kw0 + 31 > qbase) || kw0 + 32 > S) {   // wave-uniform
+      if ((causal && kw0 + 31 > qh) || kw0 + 32 > S) {   // wave-uniform
         // key > query (causal) or key past S -> P = 0
         const int qlim = causal ? mykey : 0;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int q = qbase + 8 * (r >> 2) + 4 * g + (r & 3);
+          const int q = qh + 8 * (r >> 2) + 4 * g + (r & 3);
           p[r] = ((q < qlim) | (mykey >= S)) ? 0.f : p[r];
         }
       }
@@ -254,11 +260,12 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
       for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          dvacc[db] = mfma32(RT::template tr_frag<true>(dos, kc * 16, db * 32, lane), pp[kc],
-                             dvacc[db]);
-          dkacc[db] = mfma32(RT::template tr_frag<true>(qs, kc * 16, db * 32, lane), pds[kc],
-                             dkacc[db]);
+          dvacc[db] = mfma32(RT::template tr_frag<true>(dos, hq * 32 + kc * 16, db * 32, lane),
+                             pp[kc], dvacc[db]);
+          dkacc[db] = mfma32(RT::template tr_frag<true>(qs, hq * 32 + kc * 16, db * 32, lane),
+                             pds[kc], dkacc[db]);
         }
+    }
     }
 
     // next block resident for every wave; nobody reads this buffer any more
@@ -510,7 +517,7 @@ hipError_t launch_bwd(const AttnBwdArgs& a, hipStream_t s) {
   if (e != hipSuccess) return e;
   const int n_kt = (sh.S + BKV - 1) / BKV;
   hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D>),
-                     dim3((unsigned)(n_kt * sh.B * sh.Hkv * a.nsplit)), dim3(NW * 64), 0, s, a.Q,
+                     dim3((unsigned)(n_kt * sh.B * sh.Hkv * a.nsplit)), dim3(NWA * 64), 0, s, a.Q,
                      a.K, a.V, a.q_stride, a.kv_stride, a.dO, a.o_stride, a.lse2, a.delta, a.dK,
                      a.dV, a.dkv_stride, a.part, a.nsplit, sh.B, sh.S, sh.Hq, sh.Hkv, sh.scale,
                      sh.causal);

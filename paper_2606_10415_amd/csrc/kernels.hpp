@@ -67,15 +67,16 @@ inline size_t attn_bwd_delta_bytes(int B, int S, int Hq) {
   return align256((size_t)B * Hq * S * sizeof(float));
 }
 inline size_t attn_bwd_lse2_bytes(int B, int S, int Hq) { return attn_bwd_delta_bytes(B, S, Hq); }
-// The dK/dV pass runs one workgroup per (128-key tile, batch, kv head, split);
-// with grouped queries and few kv heads the Hq/Hkv query heads of a group are
-// split over the smallest divisor n of Hq/Hkv that gives at least 1024
-// workgroups (all of them if none does), each writing FP32 partial sums.
+// The dK/dV pass runs one workgroup per (256-key tile, batch, kv head, split),
+// one workgroup per CU; with grouped queries and few kv heads the Hq/Hkv
+// query heads of a group are split over the smallest divisor n of Hq/Hkv that
+// gives at least 512 workgroups (all of them if none does), each writing FP32
+// partial sums.
 inline int attn_bwd_dkdv_splits(int B, int S, int Hq, int Hkv) {
   const int grp = Hq / Hkv;
-  const int64_t wgs = (int64_t)((S + 127) / 128) * B * Hkv;
+  const int64_t wgs = (int64_t)((S + 255) / 256) * B * Hkv;
   for (int n = 1; n < grp; ++n)
-    if (grp % n == 0 && wgs * n >= 1024) return n;
+    if (grp % n == 0 && wgs * n >= 512) return n;
   return grp;
 }
 inline size_t attn_bwd_part_bytes(int B, int S, int Hq, int Hkv, int D) {
