@@ -27,9 +27,9 @@
 //                     partial dK, dV go to the workspace and are summed in a
 //                     fixed order by attn_bwd_dkdv_sum (kernel 4).
 //   3. attn_bwd_dq  : query-major, the forward's layout.  One workgroup per
-//                     (batch, head, 128-query tile); each wave owns 32 queries
+//                     (batch, head, 256-query tile, 8 waves); each wave owns 32 queries
 //                     (Q and dO fragments and the dQ accumulator in registers)
-//                     and walks the causal 64-key slices of K and V (direct
+//                     and walks the causal 128-key slices of K and V (direct
 //                     loads, double-buffered), recomputing S^T and dP^T with
 //                     one query per lane; dQ^T += K^T dS^T reads K^T through the
 //                     transpose read.  dQ is written once, in FP16.
@@ -47,9 +47,9 @@ namespace {
 constexpr int NWA = 8;         // dK/dV: waves per workgroup
 constexpr int BKV = NWA * 32;  // dK/dV: keys per workgroup (32 per wave)
 constexpr int BQA = 64;        // dK/dV: queries per block (two 32-query halves)
-constexpr int NW = 4;          // dQ: waves per workgroup
+constexpr int NW = 8;          // dQ: waves per workgroup
 constexpr int BQB = NW * 32;   // dQ: queries per workgroup (32 per wave)
-constexpr int BKB = 64;        // dQ: keys per slice
+constexpr int BKB = 128;       // dQ: keys per slice
 constexpr float kLog2e = 1.4426950408889634f;
 
 // ------------------------------------------------------------ kernel 1
