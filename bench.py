@@ -119,6 +119,95 @@ def cpu_baseline(w, budget_s=20.0):
                        f"{t_total:.1f} s, float64 numpy/OpenBLAS")}
 
 
+def sweep():
+    """Sweeps beside the headline step, one JSON line each (stdout):
+
+    * attention forward / backward at the sequence lengths of the paper's
+      attention-BP comparison (LLaMA-2-7B heads at S = 1024, 2048, 4096;
+      Qwen2.5-32B heads at S = 2048), B = 1, causal;
+    * the paper's representative GEMM shapes (Sec. 6.6, Table "Representative
+      FP16 GEMM backend profile", sequence length 2048): M = 2048 tokens,
+      K x N = 4096x4096, 4096x11008, 11008x4096, 6656x6656, 8192x8192, as the
+      forward projection C = X W^T;
+    * the whole LLaMA-2-7B-shaped layer step at S = 1024 and 2048.
+
+    Inputs are seeded normal tensors made on the device (timing only).
+    """
+    import dataclasses
+    import torch
+    from paper_2606_10415_amd import lt
+    from paper_2606_10415_amd.layer import DecoderLayer
+
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(12345)
+
+    def rand(*shape, std=1.0):
+        return (torch.randn(*shape, device="cuda", generator=gen) * std).half()
+
+    def timed(fn, iters=10, warm=3):
+        for _ in range(warm):
+            fn()
+        torch.cuda.synchronize()
+        s = torch.cuda.Event(enable_timing=True)
+        e = torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(iters):
+            fn()
+        e.record()
+        torch.cuda.synchronize()
+        return s.elapsed_time(e) / iters
+
+    def emit(d):
+        print(json.dumps(d), flush=True)
+
+    for name, B, S, Hq, Hkv, D in [("llama2-7b", 1, 1024, 32, 32, 128),
+                                   ("llama2-7b", 1, 2048, 32, 32, 128),
+                                   ("llama2-7b", 1, 4096, 32, 32, 128),
+                                   ("qwen2.5-32b", 1, 2048, 40, 8, 128)]:
+        T, W = B * S, (Hq + 2 * Hkv) * D
+        QKV, dO = rand(T, W), rand(T, Hq * D)
+        O = torch.empty(T, Hq * D, dtype=torch.float16, device="cuda")
+        dQKV = torch.empty_like(QKV)
+        LSE = torch.empty(B, Hq, S, dtype=torch.float32, device="cuda")
+        wsb = lt.lt_attn_bwd_workspace_size(B, S, Hq, Hkv, D)
+        ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+        p, dp, sc = QKV.data_ptr(), dQKV.data_ptr(), 1.0 / math.sqrt(D)
+        q, k, v = p, p + 2 * Hq * D, p + 2 * (Hq + Hkv) * D
+        dq, dk, dv = dp, dp + 2 * Hq * D, dp + 2 * (Hq + Hkv) * D
+        fwd = lambda: lt.lt_attn_fwd(q, k, v, W, W, O, Hq * D, LSE, B, S, Hq, Hkv, D, sc, 1)
+        bwd = lambda: lt.lt_attn_bwd(q, k, v, W, W, O, dO, Hq * D, LSE, dq, dk, dv, W, W, ws, wsb,
+                                     B, S, Hq, Hkv, D, sc, 1)
+        fwd()
+        pairs = S * (S + 1) // 2 * Hq * B
+        tf, tb = timed(fwd), timed(bwd)
+        emit({"sweep": "attention", "workload": name, "B": B, "S": S, "Hq": Hq, "Hkv": Hkv, "D": D,
+              "fwd_ms": round(tf, 4), "fwd_tflops": round(4 * D * pairs / tf / 1e9, 1),
+              "bwd_ms": round(tb, 4), "bwd_tflops": round(8 * D * pairs / tb / 1e9, 1),
+              "bwd_frac_peak": round(8 * D * pairs / tb / 1e9 / PEAK_FP16_TFLOPS, 4)})
+        del QKV, dO, O, dQKV, ws
+
+    M = 2048
+    for K, N in [(4096, 4096), (4096, 11008), (11008, 4096), (6656, 6656), (8192, 8192)]:
+        A, Wt = rand(M, K), rand(N, K, std=0.02)
+        C = torch.empty(M, N, dtype=torch.float16, device="cuda")
+        t = timed(lambda: lt.lt_gemm_f16(0, 1, M, N, K, 1.0, A, K, Wt, K, 0.0, C, N), iters=20)
+        tfl = 2 * M * N * K / t / 1e9
+        emit({"sweep": "gemm", "M": M, "K": K, "N": N, "layout": "NT (X W^T)", "ms": round(t, 4),
+              "tflops": round(tfl, 1), "frac_peak": round(tfl / PEAK_FP16_TFLOPS, 4)})
+        del A, Wt, C
+
+    base = WORKLOADS["llama2-7b"]
+    for S in (1024, 2048):
+        w = dataclasses.replace(base, name=f"llama2-7b-s{S}", S=S)
+        L = DecoderLayer(w, layer_inputs(w))
+        t = timed(L.step, iters=10)
+        fl = layer_flops(w)
+        emit({"sweep": "layer", "workload": w.name, "B": w.B, "S": S, "ms_per_step": round(t, 4),
+              "tflops": round(fl["total"] / t / 1e9, 1),
+              "frac_peak": round(fl["total"] / t / 1e9 / PEAK_FP16_TFLOPS, 4)})
+        del L
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -126,6 +215,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama2-7b", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the headline step, print the sequence / GEMM-shape sweeps "
+                         "(one JSON line each)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="before warmup, run a plain elementwise copy (negation) of this many "
                          "MiB of fp16 three times: the reference dispatch for scaling HBM "
@@ -140,6 +232,9 @@ def main():
     import torch
     assert torch.cuda.is_available(), "bench.py needs a ROCm GPU"
     from paper_2606_10415_amd.layer import DecoderLayer
+    if args.sweep:
+        sweep()
+        return
 
     w = WORKLOADS[args.workload]
     print(f"[bench] workload {w.name}: generating inputs", file=sys.stderr, flush=True)
