@@ -14,7 +14,10 @@ preserves the model computation exactly; Sec. 4.1 and Sec. 5.3):
                     gradient (Sec. 4.1, Algorithm 1, Memory-resident
                     Attention Backward)
 * ``swiglu``     -- SwiGLU gate of the FFN projection and its gradient
+* ``norm_rope``  -- RMSNorm and rotary position embedding of the evaluated
+                    models (Sec. 6.1) and their gradients
 * ``layer``      -- one decoder layer forward + backward composed of the above
+                    (optionally with the models' RMSNorm and rotary embedding)
 
 No blocking, fusion, online softmax or reordering: a reader can check each
 function against the definitions by eye.  Library primitives used as single
@@ -28,11 +31,13 @@ worked examples under ``tests/golden/``).
 from .gemm import gemm, gemm_entries
 from .attention import attn_fwd, attn_bwd, attn_head_fwd, attn_head_bwd
 from .swiglu import silu, swiglu_fwd, swiglu_bwd
-from .layer import LayerShape, layer_fwd, layer_bwd, layer_flops
+from .norm_rope import rmsnorm_fwd, rmsnorm_bwd, rope_angles, rope_fwd, rope_bwd
+from .layer import LayerShape, LayerNorms, layer_fwd, layer_bwd, layer_flops
 
 __all__ = [
     "gemm", "gemm_entries",
     "attn_fwd", "attn_bwd", "attn_head_fwd", "attn_head_bwd",
     "silu", "swiglu_fwd", "swiglu_bwd",
-    "LayerShape", "layer_fwd", "layer_bwd", "layer_flops",
+    "rmsnorm_fwd", "rmsnorm_bwd", "rope_angles", "rope_fwd", "rope_bwd",
+    "LayerShape", "LayerNorms", "layer_fwd", "layer_bwd", "layer_flops",
 ]

@@ -28,9 +28,11 @@ _LN = re.compile(r"ln(\d+)")
 
 
 def golden_value(expr):
-    """Evaluate a fixture expression such as '-2/9*ln2 - 30/169*ln3' in float64."""
+    """Evaluate a fixture expression such as '-2/9*ln2 - 30/169*ln3', '2**0.5/5'
+    or '3*cos(1) + sin(1)' in float64."""
     names = {f"ln{n}": math.log(int(n)) for n in _LN.findall(expr)}
-    if not re.fullmatch(r"[0-9lnN+\-*/(). ]*", expr):
+    names.update({"cos": math.cos, "sin": math.sin})
+    if not re.fullmatch(r"([0-9+\-*/(). ]|ln\d+|cos|sin)*", expr):
         raise ValueError(f"unexpected token in fixture expression {expr!r}")
     return float(eval(expr, {"__builtins__": {}}, names))  # fixture-local arithmetic only
 
