@@ -186,6 +186,64 @@ lt_status lt_swiglu_fwd(const lt_half* GU, lt_half* A, int64_t T, int64_t F,
 lt_status lt_swiglu_bwd(const lt_half* dA, const lt_half* GU, lt_half* dGU,
                         int64_t T, int64_t F, lt_stream stream);
 
+/*
+ * RMSNorm of the evaluated models' decoder layers (Sec. 6.1 names LLaMA-2,
+ * Baichuan2 and Qwen2.5; the paper itself defines no normalisation), per
+ * token row x of width H:  r = (mean_j x_j^2 + eps)^(-1/2),  y = w * x * r.
+ *   X [T, H] (row stride ldx), W [H], Y [T, H] (ldy): FP16; RSTD [T]: FP32,
+ *   the r of every row, kept for the backward.  Math in FP32, one rounding
+ *   per output.  H must be a multiple of 8 and <= 8192, strides multiples of
+ *   8 elements, pointers 16-byte aligned (else LT_ERR_UNSUPPORTED); eps
+ *   finite and >= 0.  T = 0 is a no-op.
+ */
+lt_status lt_rmsnorm_fwd(const lt_half* X, int64_t ldx, const lt_half* W,
+                         lt_half* Y, int64_t ldy, float* RSTD, int64_t T,
+                         int64_t H, float eps, lt_stream stream);
+
+/*
+ * Bytes of device workspace lt_rmsnorm_bwd needs (FP32 partial sums of dW,
+ * 256-byte aligned); 0 for invalid sizes.
+ */
+size_t lt_rmsnorm_bwd_workspace_size(int64_t T, int64_t H);
+
+/*
+ * RMSNorm backward, given dY (the gradient of y) and the forward's X, W, RSTD:
+ *   dX = R + r * w * dY - r^3 * x / H * sum_j dY_j w_j x_j   (R optional,
+ *        NULL for none: the residual-branch gradient added in the same pass),
+ *   dW = sum over rows of dY * x * r   (FP16, summed in FP32 in a fixed
+ *        order: deterministic).
+ * Layouts and limits as lt_rmsnorm_fwd; T >= 1.  `workspace` is a device
+ * buffer of at least lt_rmsnorm_bwd_workspace_size(T, H) bytes, 256-byte
+ * aligned, owned by the caller.
+ */
+lt_status lt_rmsnorm_bwd(const lt_half* dY, int64_t lddy, const lt_half* X,
+                         int64_t ldx, const lt_half* W, const float* RSTD,
+                         const lt_half* R, int64_t ldr, lt_half* dX,
+                         int64_t lddx, lt_half* dW, void* workspace,
+                         size_t ws_bytes, int64_t T, int64_t H,
+                         lt_stream stream);
+
+/*
+ * Rotary position embedding table of the evaluated models (rotate-half
+ * pairing): CS[p][i] = (cos a, sin a), a = p * base^(-2i/D), for p < S and
+ * i < D/2, FP32 pairs ([S][D/2][2], caller-owned, 16-byte aligned).  The
+ * angle is formed and reduced in FP64.  D must be a multiple of 16.
+ */
+lt_status lt_rope_table(float* CS, int S, int D, double base,
+                        lt_stream stream);
+
+/*
+ * Rotary embedding in place on `heads` consecutive heads of width D of every
+ * token row: element (b, p, h, :) at X + (b*S + p) * row_stride + h*D (in
+ * the fused QKV buffer the Q heads and then the K heads, heads = Hq + Hkv).
+ * Pairs (i, i + D/2) rotate by the angle of CS[p][i]; inverse = 1 rotates by
+ * the negated angle, which is the gradient of the forward rotation.  FP32
+ * math, one rounding per output.  D % 16 == 0, row_stride % 8 == 0, X and
+ * CS 16-byte aligned (else LT_ERR_UNSUPPORTED).
+ */
+lt_status lt_rope_f16(lt_half* X, int64_t row_stride, int B, int S, int heads,
+                      int D, const float* CS, int inverse, lt_stream stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -84,9 +84,41 @@ inline size_t attn_bwd_part_bytes(int B, int S, int Hq, int Hkv, int D) {
   return n > 1 ? align256((size_t)2 * n * B * S * Hkv * D * sizeof(float)) : 0;
 }
 
+// RMSNorm backward (norm_rope.hip).  dW partial sums: one FP32 row of H per
+// wave, 4 waves per workgroup, rmsnorm_bwd_blocks(T) workgroups.
+struct RmsBwdArgs {
+  const lt_half* dY;
+  int64_t lddy;
+  const lt_half* X;
+  int64_t ldx;
+  const lt_half* W;
+  const float* RSTD;
+  const lt_half* R;      // optional residual added to dX (may be null)
+  int64_t ldr;
+  lt_half* dX;
+  int64_t lddx;
+  lt_half* dW;
+  float* part;           // workspace
+  int64_t T, H;
+};
+inline int rmsnorm_bwd_blocks(int64_t T) {
+  const int64_t b = (T + 15) / 16;
+  return (int)(b < 256 ? (b < 1 ? 1 : b) : 256);
+}
+inline size_t rmsnorm_bwd_ws_bytes(int64_t T, int64_t H) {
+  return align256((size_t)rmsnorm_bwd_blocks(T) * 4 * H * sizeof(float));
+}
+
 hipError_t gemm_f16_launch(const GemmArgs& a, hipStream_t s);
 hipError_t attn_fwd_launch(const AttnFwdArgs& a, hipStream_t s);
 hipError_t attn_bwd_launch(const AttnBwdArgs& a, hipStream_t s);
+hipError_t rmsnorm_fwd_launch(const lt_half* X, int64_t ldx, const lt_half* W, lt_half* Y,
+                              int64_t ldy, float* RSTD, int64_t T, int64_t H, float eps,
+                              hipStream_t s);
+hipError_t rmsnorm_bwd_launch(const RmsBwdArgs& a, hipStream_t s);
+hipError_t rope_table_launch(float* CS, int S, int D, double base, hipStream_t s);
+hipError_t rope_launch(lt_half* X, int64_t stride, int B, int S, int heads, int D, const float* CS,
+                       int inverse, hipStream_t s);
 hipError_t swiglu_fwd_launch(const lt_half* GU, lt_half* A, int64_t T, int64_t F, hipStream_t s);
 hipError_t swiglu_bwd_launch(const lt_half* dA, const lt_half* GU, lt_half* dGU, int64_t T,
                              int64_t F, hipStream_t s);

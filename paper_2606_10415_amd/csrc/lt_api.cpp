@@ -177,6 +177,85 @@ lt_status lt_attn_bwd(const lt_half* Q, const lt_half* K, const lt_half* V, int6
   return from_hip(lt::attn_bwd_launch(a, reinterpret_cast<hipStream_t>(stream)), "attn_bwd launch");
 }
 
+size_t lt_rmsnorm_bwd_workspace_size(int64_t T, int64_t H) {
+  if (T < 1 || H < 1) return 0;
+  return lt::rmsnorm_bwd_ws_bytes(T, H);
+}
+
+static lt_status check_rms(int64_t T, int64_t H, int64_t lds[], int n_ld, const void* ptrs[],
+                           int n_ptr) {
+  if (T < 0 || H < 1) return fail(LT_ERR_INVALID_ARG, "T < 0 or H < 1");
+  for (int i = 0; i < n_ptr; ++i)
+    if (!ptrs[i]) return fail(LT_ERR_INVALID_ARG, "NULL pointer");
+  for (int i = 0; i < n_ld; ++i)
+    if (lds[i] < H) return fail(LT_ERR_INVALID_ARG, "row stride smaller than H");
+  if (H & 7 || H > 8192) return fail(LT_ERR_UNSUPPORTED, "H must be a multiple of 8 and <= 8192");
+  for (int i = 0; i < n_ld; ++i)
+    if (lds[i] & 7) return fail(LT_ERR_UNSUPPORTED, "row strides must be multiples of 8 elements");
+  for (int i = 0; i < n_ptr; ++i)
+    if (!aligned16(ptrs[i])) return fail(LT_ERR_UNSUPPORTED, "pointers must be 16-byte aligned");
+  return LT_OK;
+}
+
+lt_status lt_rmsnorm_fwd(const lt_half* X, int64_t ldx, const lt_half* W, lt_half* Y, int64_t ldy,
+                         float* RSTD, int64_t T, int64_t H, float eps, lt_stream stream) {
+  int64_t lds[2] = {ldx, ldy};
+  const void* ptrs[4] = {X, W, Y, RSTD};
+  lt_status st = check_rms(T, H, lds, 2, ptrs, 4);
+  if (st != LT_OK) return st;
+  if (!(eps >= 0.f) || !std::isfinite(eps)) return fail(LT_ERR_INVALID_ARG, "eps must be finite and >= 0");
+  if (T == 0) return ok();
+  return from_hip(lt::rmsnorm_fwd_launch(X, ldx, W, Y, ldy, RSTD, T, H, eps,
+                                         reinterpret_cast<hipStream_t>(stream)),
+                  "rmsnorm_fwd launch");
+}
+
+lt_status lt_rmsnorm_bwd(const lt_half* dY, int64_t lddy, const lt_half* X, int64_t ldx,
+                         const lt_half* W, const float* RSTD, const lt_half* R, int64_t ldr,
+                         lt_half* dX, int64_t lddx, lt_half* dW, void* workspace, size_t ws_bytes,
+                         int64_t T, int64_t H, lt_stream stream) {
+  int64_t lds[4] = {lddy, ldx, lddx, R ? ldr : H};
+  const void* ptrs[6] = {dY, X, W, RSTD, dX, dW};
+  lt_status st = check_rms(T, H, lds, 4, ptrs, 6);
+  if (st != LT_OK) return st;
+  if (R && !aligned16(R)) return fail(LT_ERR_UNSUPPORTED, "R must be 16-byte aligned");
+  if (T == 0) return fail(LT_ERR_INVALID_ARG, "T must be >= 1 (dW is a sum over rows)");
+  const size_t need = lt_rmsnorm_bwd_workspace_size(T, H);
+  if (!workspace || ws_bytes < need)
+    return fail(LT_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                workspace ? ws_bytes : (size_t)0);
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  lt::RmsBwdArgs a{dY, lddy, X, ldx, W, RSTD, R, ldr, dX, lddx, dW,
+                   static_cast<float*>(workspace), T, H};
+  return from_hip(lt::rmsnorm_bwd_launch(a, reinterpret_cast<hipStream_t>(stream)),
+                  "rmsnorm_bwd launch");
+}
+
+lt_status lt_rope_table(float* CS, int S, int D, double base, lt_stream stream) {
+  if (!CS) return fail(LT_ERR_INVALID_ARG, "NULL pointer");
+  if (S < 1 || D < 2) return fail(LT_ERR_INVALID_ARG, "S < 1 or D < 2");
+  if (!(base > 0.0) || !std::isfinite(base)) return fail(LT_ERR_INVALID_ARG, "base must be finite and > 0");
+  if (D & 15) return fail(LT_ERR_UNSUPPORTED, "D must be a multiple of 16");
+  if (!aligned16(CS)) return fail(LT_ERR_UNSUPPORTED, "CS must be 16-byte aligned");
+  return from_hip(lt::rope_table_launch(CS, S, D, base, reinterpret_cast<hipStream_t>(stream)),
+                  "rope_table launch");
+}
+
+lt_status lt_rope_f16(lt_half* X, int64_t row_stride, int B, int S, int heads, int D,
+                      const float* CS, int inverse, lt_stream stream) {
+  if (!X || !CS) return fail(LT_ERR_INVALID_ARG, "NULL pointer");
+  if (B < 1 || S < 1 || heads < 1 || D < 2) return fail(LT_ERR_INVALID_ARG, "non-positive size");
+  if (inverse != 0 && inverse != 1) return fail(LT_ERR_INVALID_ARG, "inverse must be 0 or 1");
+  if (row_stride < (int64_t)heads * D) return fail(LT_ERR_INVALID_ARG, "row stride smaller than heads * D");
+  if (D & 15) return fail(LT_ERR_UNSUPPORTED, "D must be a multiple of 16");
+  if ((row_stride & 7) || !aligned16(X) || !aligned16(CS))
+    return fail(LT_ERR_UNSUPPORTED, "X, CS must be 16-byte aligned and row_stride % 8 == 0");
+  return from_hip(lt::rope_launch(X, row_stride, B, S, heads, D, CS, inverse,
+                                  reinterpret_cast<hipStream_t>(stream)),
+                  "rope launch");
+}
+
 lt_status lt_swiglu_fwd(const lt_half* GU, lt_half* A, int64_t T, int64_t F, lt_stream stream) {
   if (T < 0 || F < 0) return fail(LT_ERR_INVALID_ARG, "negative size");
   if (T == 0 || F == 0) return ok();

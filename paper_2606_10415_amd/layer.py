@@ -10,6 +10,12 @@ Forward  : QKV = X Wqkv^T ; (O, LSE) = attn(QKV) ; H1 = X + O Wo^T ;
 Backward : dWd = dY^T A ; dA = dY Wd ; dGU = swiglu_bwd ; dWgu = dGU^T H1 ;
            dH1 = dY + dGU Wgu ; dWo = dH1^T O ; dO = dH1 Wo ;
            dQKV = attn_bwd ; dWqkv = dQKV^T X ; dX = dH1 + dQKV Wqkv
+
+With ``norm`` the layer is the full block of the evaluated models: X and H1
+are RMSNorm-ed before the QKV and gate/up projections (Xn, H1n), Q and K are
+rotated in place in QKV, and the backward runs the inverse rotation on dQ, dK
+and RMSNorm backward (with the residual gradient added in the same pass):
+    dH1 = dY + rmsnorm_bwd(dGU Wgu) ;  dX = dH1 + rmsnorm_bwd(dQKV Wqkv)
 """
 
 import math
@@ -23,10 +29,11 @@ class DecoderLayer:
     """Device buffers and the liblt call sequence of one layer.
 
     ``shape`` needs attributes B, S, H, Hq, Hkv, D, F.  ``params`` maps
-    X, dY, Wqkv, Wo, Wgu, Wd to float16 tensors (host or device).
+    X, dY, Wqkv, Wo, Wgu, Wd to float16 tensors (host or device).  ``norm``
+    (optional) has attributes wn1, wn2 (RMSNorm weights [H]), eps, rope_base.
     """
 
-    def __init__(self, shape, params, device="cuda"):
+    def __init__(self, shape, params, device="cuda", norm=None):
         self.sh = sh = shape
         self.dev = torch.device(device)
         T = sh.B * sh.S
@@ -67,6 +74,25 @@ class DecoderLayer:
         self.ws_bytes = lt.lt_attn_bwd_workspace_size(sh.B, sh.S, sh.Hq, sh.Hkv, sh.D)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.dev)
 
+        self.norm = norm
+        if norm is not None:
+            self.eps = float(norm.eps)
+            self.Wn1 = dev(norm.wn1)
+            self.Wn2 = dev(norm.wn2)
+            self.Xn = e(T, sh.H)
+            self.H1n = e(T, sh.H)
+            self.dXn = e(T, sh.H)
+            self.dH1n = e(T, sh.H)
+            self.dWn1 = e(sh.H)
+            self.dWn2 = e(sh.H)
+            f32 = lambda *s_: torch.empty(*s_, dtype=torch.float32, device=self.dev)
+            self.rstd1 = f32(T)
+            self.rstd2 = f32(T)
+            self.CS = f32(sh.S, sh.D // 2, 2)
+            lt.lt_rope_table(self.CS, sh.S, sh.D, float(norm.rope_base))
+            self.rms_ws_bytes = lt.lt_rmsnorm_bwd_workspace_size(T, sh.H)
+            self.rms_ws = torch.empty(self.rms_ws_bytes, dtype=torch.uint8, device=self.dev)
+
     # ------------------------------------------------------------ steps
     def _attn_ptrs(self, base):
         p = base.data_ptr()
@@ -76,9 +102,18 @@ class DecoderLayer:
         """Layer forward.  ``hook(name)`` (optional) is called after each launch."""
         sh, T = self.sh, self.T
         mark = hook or (lambda name: None)
-        lt.lt_gemm_f16(0, 1, T, self.qkv, sh.H, 1.0, self.X, sh.H, self.Wqkv, sh.H, 0.0,
+        xin = self.X
+        if self.norm is not None:
+            lt.lt_rmsnorm_fwd(self.X, sh.H, self.Wn1, self.Xn, sh.H, self.rstd1, T, sh.H, self.eps,
+                              stream)
+            mark("rmsnorm1_fwd")
+            xin = self.Xn
+        lt.lt_gemm_f16(0, 1, T, self.qkv, sh.H, 1.0, xin, sh.H, self.Wqkv, sh.H, 0.0,
                        self.QKV, self.qkv, stream)
         mark("qkv_fwd")
+        if self.norm is not None:
+            lt.lt_rope_f16(self.QKV, self.qkv, sh.B, sh.S, sh.Hq + sh.Hkv, sh.D, self.CS, 0, stream)
+            mark("rope_fwd")
         q, k, v = self._attn_ptrs(self.QKV)
         lt.lt_attn_fwd(q, k, v, self.qkv, self.qkv, self.O, self.hd, self.LSE, sh.B, sh.S, sh.Hq,
                        sh.Hkv, sh.D, self.scale, 1, stream)
@@ -86,7 +121,13 @@ class DecoderLayer:
         lt.lt_gemm_f16_res(0, 1, T, sh.H, self.hd, 1.0, self.O, self.hd, self.Wo, self.hd, 1.0,
                            self.X, sh.H, self.H1, sh.H, stream)
         mark("o_fwd")
-        lt.lt_gemm_f16(0, 1, T, 2 * sh.F, sh.H, 1.0, self.H1, sh.H, self.Wgu, sh.H, 0.0, self.GU,
+        hin = self.H1
+        if self.norm is not None:
+            lt.lt_rmsnorm_fwd(self.H1, sh.H, self.Wn2, self.H1n, sh.H, self.rstd2, T, sh.H,
+                              self.eps, stream)
+            mark("rmsnorm2_fwd")
+            hin = self.H1n
+        lt.lt_gemm_f16(0, 1, T, 2 * sh.F, sh.H, 1.0, hin, sh.H, self.Wgu, sh.H, 0.0, self.GU,
                        2 * sh.F, stream)
         mark("gu_fwd")
         lt.lt_swiglu_fwd(self.GU, self.A, T, sh.F, stream)
@@ -108,12 +149,22 @@ class DecoderLayer:
         lt.lt_swiglu_bwd(self.dA, self.GU, self.dGU, T, sh.F, stream)
         mark("swiglu_bwd")
         # gate/up projection
-        lt.lt_gemm_f16(1, 0, 2 * sh.F, sh.H, T, 1.0, self.dGU, 2 * sh.F, self.H1, sh.H, 0.0,
+        hin = self.H1n if self.norm is not None else self.H1
+        lt.lt_gemm_f16(1, 0, 2 * sh.F, sh.H, T, 1.0, self.dGU, 2 * sh.F, hin, sh.H, 0.0,
                        self.dWgu, sh.H, stream)
         mark("gu_wgrad")
-        lt.lt_gemm_f16_res(0, 0, T, sh.H, 2 * sh.F, 1.0, self.dGU, 2 * sh.F, self.Wgu, sh.H, 1.0,
-                           self.dY, sh.H, self.dH1, sh.H, stream)
-        mark("gu_dgrad")
+        if self.norm is not None:
+            lt.lt_gemm_f16(0, 0, T, sh.H, 2 * sh.F, 1.0, self.dGU, 2 * sh.F, self.Wgu, sh.H, 0.0,
+                           self.dH1n, sh.H, stream)
+            mark("gu_dgrad")
+            lt.lt_rmsnorm_bwd(self.dH1n, sh.H, self.H1, sh.H, self.Wn2, self.rstd2, self.dY, sh.H,
+                              self.dH1, sh.H, self.dWn2, self.rms_ws, self.rms_ws_bytes, T, sh.H,
+                              stream)
+            mark("rmsnorm2_bwd")
+        else:
+            lt.lt_gemm_f16_res(0, 0, T, sh.H, 2 * sh.F, 1.0, self.dGU, 2 * sh.F, self.Wgu, sh.H,
+                               1.0, self.dY, sh.H, self.dH1, sh.H, stream)
+            mark("gu_dgrad")
         # output projection
         lt.lt_gemm_f16(1, 0, sh.H, self.hd, T, 1.0, self.dH1, sh.H, self.O, self.hd, 0.0, self.dWo,
                        self.hd, stream)
@@ -128,13 +179,26 @@ class DecoderLayer:
                        self.qkv, self.qkv, self.ws, self.ws_bytes, sh.B, sh.S, sh.Hq, sh.Hkv, sh.D,
                        self.scale, 1, stream)
         mark("attn_bwd")
+        if self.norm is not None:
+            lt.lt_rope_f16(self.dQKV, self.qkv, sh.B, sh.S, sh.Hq + sh.Hkv, sh.D, self.CS, 1, stream)
+            mark("rope_bwd")
         # QKV projection
-        lt.lt_gemm_f16(1, 0, self.qkv, sh.H, T, 1.0, self.dQKV, self.qkv, self.X, sh.H, 0.0,
+        xin = self.Xn if self.norm is not None else self.X
+        lt.lt_gemm_f16(1, 0, self.qkv, sh.H, T, 1.0, self.dQKV, self.qkv, xin, sh.H, 0.0,
                        self.dWqkv, sh.H, stream)
         mark("qkv_wgrad")
-        lt.lt_gemm_f16_res(0, 0, T, sh.H, self.qkv, 1.0, self.dQKV, self.qkv, self.Wqkv, sh.H, 1.0,
-                           self.dH1, sh.H, self.dX, sh.H, stream)
-        mark("qkv_dgrad")
+        if self.norm is not None:
+            lt.lt_gemm_f16(0, 0, T, sh.H, self.qkv, 1.0, self.dQKV, self.qkv, self.Wqkv, sh.H, 0.0,
+                           self.dXn, sh.H, stream)
+            mark("qkv_dgrad")
+            lt.lt_rmsnorm_bwd(self.dXn, sh.H, self.X, sh.H, self.Wn1, self.rstd1, self.dH1, sh.H,
+                              self.dX, sh.H, self.dWn1, self.rms_ws, self.rms_ws_bytes, T, sh.H,
+                              stream)
+            mark("rmsnorm1_bwd")
+        else:
+            lt.lt_gemm_f16_res(0, 0, T, sh.H, self.qkv, 1.0, self.dQKV, self.qkv, self.Wqkv, sh.H,
+                               1.0, self.dH1, sh.H, self.dX, sh.H, stream)
+            mark("qkv_dgrad")
 
     def step(self, stream=None, hook=None):
         self.forward(stream, hook)

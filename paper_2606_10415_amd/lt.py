@@ -86,6 +86,17 @@ _lib.lt_swiglu_fwd.restype = _int
 _lib.lt_swiglu_fwd.argtypes = [_vp, _vp, _i64, _i64, _vp]
 _lib.lt_swiglu_bwd.restype = _int
 _lib.lt_swiglu_bwd.argtypes = [_vp, _vp, _vp, _i64, _i64, _vp]
+_lib.lt_rmsnorm_fwd.restype = _int
+_lib.lt_rmsnorm_fwd.argtypes = [_vp, _i64, _vp, _vp, _i64, _vp, _i64, _i64, _f32, _vp]
+_lib.lt_rmsnorm_bwd_workspace_size.restype = _sz
+_lib.lt_rmsnorm_bwd_workspace_size.argtypes = [_i64, _i64]
+_lib.lt_rmsnorm_bwd.restype = _int
+_lib.lt_rmsnorm_bwd.argtypes = [_vp, _i64, _vp, _i64, _vp, _vp, _vp, _i64, _vp, _i64, _vp, _vp, _sz,
+                                _i64, _i64, _vp]
+_lib.lt_rope_table.restype = _int
+_lib.lt_rope_table.argtypes = [_vp, _int, _int, ctypes.c_double, _vp]
+_lib.lt_rope_f16.restype = _int
+_lib.lt_rope_f16.argtypes = [_vp, _i64, _int, _int, _int, _int, _vp, _int, _vp]
 
 
 def status_string(status):
@@ -167,6 +178,32 @@ def lt_swiglu_fwd(GU, A, T, F, stream=None):
 def lt_swiglu_bwd(dA, GU, dGU, T, F, stream=None):
     _check(_lib.lt_swiglu_bwd(_ptr(dA), _ptr(GU), _ptr(dGU), int(T), int(F), _stream(stream)),
            "lt_swiglu_bwd")
+
+
+def lt_rmsnorm_fwd(X, ldx, W, Y, ldy, RSTD, T, H, eps, stream=None):
+    _check(_lib.lt_rmsnorm_fwd(_ptr(X), int(ldx), _ptr(W), _ptr(Y), int(ldy), _ptr(RSTD), int(T),
+                               int(H), float(eps), _stream(stream)), "lt_rmsnorm_fwd")
+
+
+def lt_rmsnorm_bwd_workspace_size(T, H):
+    return int(_lib.lt_rmsnorm_bwd_workspace_size(int(T), int(H)))
+
+
+def lt_rmsnorm_bwd(dY, lddy, X, ldx, W, RSTD, R, ldr, dX, lddx, dW, workspace, ws_bytes, T, H,
+                   stream=None):
+    _check(_lib.lt_rmsnorm_bwd(_ptr(dY), int(lddy), _ptr(X), int(ldx), _ptr(W), _ptr(RSTD),
+                               _ptr(R), int(ldr), _ptr(dX), int(lddx), _ptr(dW), _ptr(workspace),
+                               int(ws_bytes), int(T), int(H), _stream(stream)), "lt_rmsnorm_bwd")
+
+
+def lt_rope_table(CS, S, D, base, stream=None):
+    _check(_lib.lt_rope_table(_ptr(CS), int(S), int(D), float(base), _stream(stream)),
+           "lt_rope_table")
+
+
+def lt_rope_f16(X, row_stride, B, S, heads, D, CS, inverse, stream=None):
+    _check(_lib.lt_rope_f16(_ptr(X), int(row_stride), int(B), int(S), int(heads), int(D), _ptr(CS),
+                            int(inverse), _stream(stream)), "lt_rope_f16")
 
 
 def declared_functions():

@@ -50,7 +50,21 @@ WORKLOADS = {
 }
 
 TENSOR_INDEX = {"X": 0, "dY": 1, "Wqkv": 2, "Wo": 3, "Wgu": 4, "Wd": 5,
-                "Q": 6, "K": 7, "V": 8, "dO": 9}
+                "Q": 6, "K": 7, "V": 8, "dO": 9, "Wn1": 10, "Wn2": 11}
+
+
+@dataclass(frozen=True)
+class NormInputs:
+    """RMSNorm weights [H] of the attention and FFN inputs, eps and rotary base."""
+    wn1: np.ndarray
+    wn2: np.ndarray
+    eps: float
+    rope_base: float
+
+
+# eps and rotary base of the evaluated model families (their published
+# configurations): LLaMA-2 and Baichuan2 1e-5 / 1e4 ("llama"), Qwen2.5 1e-6 / 1e6.
+NORM_CONSTANTS = {"llama": (1e-5, 10000.0), "qwen": (1e-6, 1000000.0)}
 
 
 def normal_f16(seed, shape, std=1.0):
@@ -80,6 +94,16 @@ def layer_inputs(w):
         "Wgu": normal_f16(base + t["Wgu"], (2 * w.F, w.H), 0.02),
         "Wd": normal_f16(base + t["Wd"], (w.H, w.F), 0.02),
     }
+
+
+def norm_inputs(w, family="llama"):
+    """RMSNorm weights 1 + N(0, 0.1^2) (float16) for workload ``w`` and the
+    family's eps and rotary base."""
+    base = 1000 * w.index
+    t = TENSOR_INDEX
+    eps, rope_base = NORM_CONSTANTS[family]
+    one = lambda seed: (1.0 + normal_f16(seed, (w.H,), 0.1).astype(np.float32)).astype(np.float16)
+    return NormInputs(one(base + t["Wn1"]), one(base + t["Wn2"]), eps, rope_base)
 
 
 def attention_inputs(B, S, Hq, Hkv, D, seed_base=0, qk_std=1.0):

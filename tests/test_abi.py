@@ -13,7 +13,9 @@ def test_every_declared_symbol_is_exported():
     names = lt.declared_functions()
     assert {"lt_gemm_f16", "lt_gemm_f16_res", "lt_attn_fwd", "lt_attn_bwd",
             "lt_attn_bwd_workspace_size", "lt_swiglu_fwd", "lt_swiglu_bwd",
-            "lt_status_string", "lt_last_error", "lt_version"} <= set(names)
+            "lt_status_string", "lt_last_error", "lt_version", "lt_rmsnorm_fwd",
+            "lt_rmsnorm_bwd", "lt_rmsnorm_bwd_workspace_size", "lt_rope_table",
+            "lt_rope_f16"} <= set(names)
     for n in names:
         assert hasattr(lt._lib, n), f"{n} declared in lt.h but not exported"
 
@@ -137,3 +139,69 @@ def test_errors_raise_lt_error():
     with pytest.raises(lt.LtError) as e:
         lt.lt_gemm_f16(0, 1, -1, 8, 8, 1.0, FAKE, 8, FAKE, 8, 0.0, FAKE, 8, stream=0)
     assert e.value.status == lt.LT_ERR_INVALID_ARG
+
+
+def _rms_fwd(**kw):
+    a = dict(X=FAKE, ldx=4096, W=FAKE, Y=FAKE, ldy=4096, RSTD=FAKE, T=16, H=4096, eps=1e-5)
+    a.update(kw)
+    return lt._lib.lt_rmsnorm_fwd(a["X"], a["ldx"], a["W"], a["Y"], a["ldy"], a["RSTD"], a["T"],
+                                  a["H"], a["eps"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(X=None), lt.LT_ERR_INVALID_ARG),
+    (dict(H=0), lt.LT_ERR_INVALID_ARG),
+    (dict(T=-1), lt.LT_ERR_INVALID_ARG),
+    (dict(ldx=132, H=128), lt.LT_ERR_UNSUPPORTED),     # stride not a multiple of 8
+    (dict(ldy=64, H=128), lt.LT_ERR_INVALID_ARG),      # stride below the row
+    (dict(H=12, ldx=16, ldy=16), lt.LT_ERR_UNSUPPORTED),
+    (dict(H=16384, ldx=16384, ldy=16384), lt.LT_ERR_UNSUPPORTED),
+    (dict(eps=-1.0), lt.LT_ERR_INVALID_ARG),
+    (dict(eps=float("nan")), lt.LT_ERR_INVALID_ARG),
+    (dict(Y=FAKE + 8), lt.LT_ERR_UNSUPPORTED),
+])
+def test_rmsnorm_fwd_rejects_on_host(kw, status):
+    assert _rms_fwd(**kw) == status
+    assert lt.last_error()
+
+
+def test_rmsnorm_empty_is_noop_and_workspace():
+    assert _rms_fwd(T=0) == lt.LT_OK
+    ws = lt.lt_rmsnorm_bwd_workspace_size(4096, 4096)
+    # 256 workgroups x 4 waves x one FP32 row of H partial sums
+    assert ws == 256 * 4 * 4096 * 4
+    assert lt.lt_rmsnorm_bwd_workspace_size(3, 8) % 256 == 0
+    assert lt.lt_rmsnorm_bwd_workspace_size(0, 8) == 0
+    st = lt._lib.lt_rmsnorm_bwd(FAKE, 4096, FAKE, 4096, FAKE, FAKE, None, 0, FAKE, 4096, FAKE,
+                                FAKE, ws - 1, 4096, 4096, None)
+    assert st == lt.LT_ERR_WORKSPACE
+    st = lt._lib.lt_rmsnorm_bwd(FAKE, 4096, FAKE, 4096, FAKE, FAKE, FAKE + 8, 4096, FAKE, 4096,
+                                FAKE, FAKE, ws, 4096, 4096, None)
+    assert st == lt.LT_ERR_UNSUPPORTED                 # misaligned residual
+
+
+@pytest.mark.parametrize("args,status", [
+    ((None, 16, 128, 1e4), lt.LT_ERR_INVALID_ARG),
+    ((FAKE, 0, 128, 1e4), lt.LT_ERR_INVALID_ARG),
+    ((FAKE, 16, 24, 1e4), lt.LT_ERR_UNSUPPORTED),      # D not a multiple of 16
+    ((FAKE, 16, 128, 0.0), lt.LT_ERR_INVALID_ARG),
+    ((FAKE, 16, 128, float("inf")), lt.LT_ERR_INVALID_ARG),
+])
+def test_rope_table_rejects_on_host(args, status):
+    assert lt._lib.lt_rope_table(*args, None) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(inverse=2), lt.LT_ERR_INVALID_ARG),
+    (dict(stride=1000), lt.LT_ERR_INVALID_ARG),        # below heads * D
+    (dict(stride=6148), lt.LT_ERR_UNSUPPORTED),        # not a multiple of 8
+    (dict(D=72, stride=72 * 40), lt.LT_ERR_UNSUPPORTED),
+    (dict(B=0), lt.LT_ERR_INVALID_ARG),
+    (dict(CS=None), lt.LT_ERR_INVALID_ARG),
+])
+def test_rope_rejects_on_host(kw, status):
+    a = dict(X=FAKE, stride=6144, B=1, S=16, heads=40, D=128, CS=FAKE, inverse=0)
+    a.update(kw)
+    st = lt._lib.lt_rope_f16(a["X"], a["stride"], a["B"], a["S"], a["heads"], a["D"], a["CS"],
+                             a["inverse"], None)
+    assert st == status

@@ -1,0 +1,119 @@
+"""GPU parity of RMSNorm, the rotary embedding and the full (normed, rotated)
+decoder layer against the float64 oracle.
+
+Bars: per op (same fp16 inputs) RMSNorm y, dx, dw and the rotated Q/K
+relative Frobenius error <= 5e-3 (one fp16 rounding of an FP32 result);
+RMSNorm rstd <= 1e-5 relative (FP32 sums); rotation table <= 1e-6 absolute
+(FP32 rounding of FP64 cos/sin); V columns of the fused buffer untouched
+(bitwise).  Chained full layer (fp16 intermediates on the GPU, float64 in the
+oracle): Y, dX, the four projection weight gradients and both RMSNorm weight
+gradients <= 5e-3, dQKV <= 1e-2.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_10415_amd.synth import (WORKLOADS, Workload, layer_inputs, norm_inputs,
+                                        normal_f16)
+from conftest import rel_f
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a ROCm device"
+    from paper_2606_10415_amd import lt
+    return torch, lt
+
+
+@pytest.mark.parametrize("T,H,residual", [(77, 5120, True), (256, 256, False), (4096, 4096, True),
+                                          (3, 8192, True), (1, 8, False)])
+def test_rmsnorm_parity(env, T, H, residual):
+    print(f"rmsnorm T={T} H={H} residual={residual}", flush=True)
+    torch, lt = env
+    x = normal_f16(41, (T, H), 2.0)
+    w = (1 + normal_f16(42, (H,), 0.1).astype(np.float32)).astype(np.float16)
+    dy = normal_f16(43, (T, H))
+    r = normal_f16(44, (T, H)) if residual else None
+    eps = 1e-5
+    cu = lambda a: torch.from_numpy(a).cuda()
+    X, Wt, dY = cu(x), cu(w), cu(dy)
+    R = cu(r) if residual else None
+    Y = torch.empty(T, H, dtype=torch.float16, device="cuda")
+    RSTD = torch.empty(T, dtype=torch.float32, device="cuda")
+    dX = torch.empty(T, H, dtype=torch.float16, device="cuda")
+    dW = torch.empty(H, dtype=torch.float16, device="cuda")
+    wsb = lt.lt_rmsnorm_bwd_workspace_size(T, H)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    lt.lt_rmsnorm_fwd(X, H, Wt, Y, H, RSTD, T, H, eps)
+    lt.lt_rmsnorm_bwd(dY, H, X, H, Wt, RSTD, R, H, dX, H, dW, ws, wsb, T, H)
+    torch.cuda.synchronize()
+    y_ref, rstd_ref = oracle.rmsnorm_fwd(x, w, eps)
+    dx_ref, dw_ref = oracle.rmsnorm_bwd(dy, x, w, eps)
+    if residual:
+        dx_ref = dx_ref + r.astype(np.float64)
+    assert rel_f(Y.cpu().numpy(), y_ref) <= 5e-3
+    assert np.max(np.abs(RSTD.cpu().numpy() / rstd_ref - 1)) <= 1e-5
+    assert rel_f(dX.cpu().numpy(), dx_ref) <= 5e-3
+    assert rel_f(dW.cpu().numpy(), dw_ref) <= 5e-3
+
+
+@pytest.mark.parametrize("B,S,Hq,Hkv,D,base", [(2, 77, 6, 2, 128, 10000.0), (1, 300, 4, 4, 64, 1e6),
+                                              (1, 4096, 8, 8, 128, 10000.0)])
+def test_rope_parity(env, B, S, Hq, Hkv, D, base):
+    print(f"rope B={B} S={S} Hq={Hq} Hkv={Hkv} D={D} base={base}", flush=True)
+    torch, lt = env
+    T, W = B * S, (Hq + 2 * Hkv) * D
+    qkv = normal_f16(51, (T, W), 1.5)
+    CS = torch.empty(S, D // 2, 2, dtype=torch.float32, device="cuda")
+    lt.lt_rope_table(CS, S, D, base)
+    X = torch.from_numpy(qkv).cuda()
+    lt.lt_rope_f16(X, W, B, S, Hq + Hkv, D, CS, 0)
+    Xi = torch.from_numpy(qkv).cuda()
+    lt.lt_rope_f16(Xi, W, B, S, Hq + Hkv, D, CS, 1)
+    torch.cuda.synchronize()
+    ang = oracle.rope_angles(S, D, base)
+    cs = CS.cpu().numpy()
+    assert np.max(np.abs(cs[..., 0] - np.cos(ang))) <= 1e-6
+    assert np.max(np.abs(cs[..., 1] - np.sin(ang))) <= 1e-6
+    qk = qkv[:, :(Hq + Hkv) * D].reshape(B, S, Hq + Hkv, D)
+    got = X.cpu().numpy()
+    goti = Xi.cpu().numpy()
+    assert rel_f(got[:, :(Hq + Hkv) * D].reshape(B, S, Hq + Hkv, D), oracle.rope_fwd(qk, base)) <= 5e-3
+    assert rel_f(goti[:, :(Hq + Hkv) * D].reshape(B, S, Hq + Hkv, D), oracle.rope_bwd(qk, base)) <= 5e-3
+    v = qkv[:, (Hq + Hkv) * D:]
+    assert np.array_equal(got[:, (Hq + Hkv) * D:].view(np.uint16), v.view(np.uint16))
+    assert np.array_equal(goti[:, (Hq + Hkv) * D:].view(np.uint16), v.view(np.uint16))
+
+
+@pytest.mark.parametrize("w,family", [(WORKLOADS["tiny"], "llama"),
+                                      (Workload("tiny-gqa", 10, B=2, S=136, H=256, Hq=4, Hkv=2,
+                                                D=64, F=344), "qwen")],
+                         ids=["tiny-llama", "tiny-gqa-ragged-qwen"])
+def test_full_layer_chained_parity(env, w, family):
+    """RMSNorm + rotary embedding + attention + SwiGLU MLP, fwd and bwd, chained."""
+    print(f"full layer chained {w.name} {family}", flush=True)
+    torch, lt = env
+    from paper_2606_10415_amd.layer import DecoderLayer
+    p = layer_inputs(w)
+    n = norm_inputs(w, family)
+    L = DecoderLayer(w, p, norm=n)
+    L.step()
+    torch.cuda.synchronize()
+    sh = oracle.LayerShape(w.B, w.S, w.H, w.Hq, w.Hkv, w.D, w.F)
+    norms = oracle.LayerNorms(wn1=n.wn1.astype(np.float64), wn2=n.wn2.astype(np.float64),
+                              eps=n.eps, rope_base=n.rope_base)
+    acts = oracle.layer_fwd(sh, p["X"], p["Wqkv"], p["Wo"], p["Wgu"], p["Wd"], norm=norms)
+    grads = oracle.layer_bwd(sh, p["X"], p["Wqkv"], p["Wo"], p["Wgu"], p["Wd"], p["dY"], acts,
+                             norm=norms)
+    c = lambda t: t.cpu().numpy()
+    err = {"Y": rel_f(c(L.Y), acts["Y"]), "dX": rel_f(c(L.dX), grads["dX"])}
+    for name in ("dWqkv", "dWo", "dWgu", "dWd", "dWn1", "dWn2"):
+        err[name] = rel_f(c(getattr(L, name)), grads[name])
+    err["dQKV"] = rel_f(c(L.dQKV), grads["dQKV"])
+    print("  errors: " + ", ".join(f"{k} {v:.3e}" for k, v in err.items()), flush=True)
+    for k, v in err.items():
+        assert v <= (1e-2 if k == "dQKV" else 5e-3), k
