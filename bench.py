@@ -26,7 +26,7 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from paper_2606_10415_amd.synth import WORKLOADS, layer_inputs  # noqa: E402
+from paper_2606_10415_amd.synth import WORKLOADS, layer_inputs, norm_inputs  # noqa: E402
 
 PEAK_FP16_TFLOPS = 2516.6     # MI355X dense FP16 MFMA (256 CU x 2.4 GHz x 4096 FLOP/clk)
 PEAK_HBM_GBS = 8000.0
@@ -215,6 +215,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="llama2-7b", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layer", default="paper", choices=["paper", "full"],
+                    help="paper: the layer of the paper's hot path (projections, attention, "
+                         "SwiGLU, residuals); full: plus the evaluated models' RMSNorm and "
+                         "rotary embedding (same FLOP count, longer step)")
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the headline step, print the sequence / GEMM-shape sweeps "
                          "(one JSON line each)")
@@ -238,7 +242,9 @@ def main():
 
     w = WORKLOADS[args.workload]
     print(f"[bench] workload {w.name}: generating inputs", file=sys.stderr, flush=True)
-    L = DecoderLayer(w, layer_inputs(w))
+    full = args.layer == "full"
+    norm = norm_inputs(w, "qwen" if w.name.startswith("qwen") else "llama") if full else None
+    L = DecoderLayer(w, layer_inputs(w), norm=norm)
     stream = torch.cuda.current_stream()
     fl = layer_flops(w)
 
@@ -317,6 +323,10 @@ def main():
         "step_ms_min": round(float(np.min(step_ms)), 4),
         "step_ms_max": round(float(np.max(step_ms)), 4),
         "per_op_ms": {k: round(v, 4) for k, v in avg.items()},
+        **({"rmsnorm_fwd_gbs": round(2 * (4 * w.T * w.H) / ((avg["rmsnorm1_fwd"] + avg["rmsnorm2_fwd"]) * 1e-3) / 1e9, 1),
+            "rmsnorm_bwd_gbs": round(2 * (8 * w.T * w.H) / ((avg["rmsnorm1_bwd"] + avg["rmsnorm2_bwd"]) * 1e-3) / 1e9, 1),
+            "rope_gbs": round(2 * (4 * w.T * (w.Hq + w.Hkv) * w.D) / ((avg["rope_fwd"] + avg["rope_bwd"]) * 1e-3) / 1e9, 1)}
+           if full else {}),
         "wall_s": round(wall, 3),
     }
     print("[bench] " + json.dumps(detail), file=sys.stderr, flush=True)
@@ -339,7 +349,9 @@ def main():
         "vs_baseline": None,
         "dtype": "f16",
         "data": "synthetic (seeded N(0,1) activations/grads, N(0,0.02^2) weights, fp16)",
-        "config": {"workload": f"{w.name} decoder layer fwd+bwd", "B": w.B, "S": w.S, "H": w.H,
+        "config": {"workload": f"{w.name} decoder layer fwd+bwd"
+                               + (" (with RMSNorm and rotary embedding)" if full else ""),
+                   "B": w.B, "S": w.S, "H": w.H,
                    "Hq": w.Hq, "Hkv": w.Hkv, "D": w.D, "F": w.F, "causal": True,
                    "flops_per_step": fl["total"], "parallelism": "single GPU"},
         "frac_of_peak": round(value / PEAK_FP16_TFLOPS, 4),

@@ -147,14 +147,28 @@ rmsnorm_bwd_kernel(const lt_half* __restrict__ dY, int64_t lddy, const lt_half* 
   }
 }
 
-// dW[j] = sum over the partial rows, in order; FP16 result.
-__global__ void __launch_bounds__(256)
+// dW[j] = sum over the partial rows; FP16 result.  Workgroup = 16 waves over
+// 64 columns (lane = column, coalesced): wave v sums partial rows v, v + 16,
+// ... in order, then wave 0 adds the 16 wave sums in order (deterministic).
+constexpr int kSumWaves = 16;
+
+__global__ void __launch_bounds__(64 * kSumWaves)
 rmsnorm_dw_sum_kernel(const float* __restrict__ part, int nparts, int H, lt_half* __restrict__ dW) {
-  const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  if (j >= H) return;
+  __shared__ float red[kSumWaves][64];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int j = blockIdx.x * 64 + lane;
   float s = 0.f;
-  for (int t = 0; t < nparts; ++t) s += part[(int64_t)t * H + j];
-  reinterpret_cast<_Float16*>(dW)[j] = (_Float16)s;
+  if (j < H)
+    for (int t = wave; t < nparts; t += kSumWaves) s += part[(int64_t)t * H + j];
+  red[wave][lane] = s;
+  __syncthreads();
+  if (wave == 0 && j < H) {
+    float tot = 0.f;
+#pragma unroll
+    for (int v = 0; v < kSumWaves; ++v) tot += red[v][lane];
+    reinterpret_cast<_Float16*>(dW)[j] = (_Float16)tot;
+  }
 }
 
 // ---------------------------------------------------------------- rotary
@@ -227,8 +241,8 @@ hipError_t launch_rms_bwd(const RmsBwdArgs& a, hipStream_t s) {
                      (int)a.H, rows_per_wg);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(rmsnorm_dw_sum_kernel, dim3((unsigned)((a.H + 255) / 256)), dim3(256), 0, s,
-                     a.part, nblk * kRowsPerWg, (int)a.H, a.dW);
+  hipLaunchKernelGGL(rmsnorm_dw_sum_kernel, dim3((unsigned)((a.H + 63) / 64)), dim3(64 * kSumWaves),
+                     0, s, a.part, nblk * kRowsPerWg, (int)a.H, a.dW);
   return hipGetLastError();
 }
 
