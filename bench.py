@@ -219,6 +219,9 @@ def main():
                     help="paper: the layer of the paper's hot path (projections, attention, "
                          "SwiGLU, residuals); full: plus the evaluated models' RMSNorm and "
                          "rotary embedding (same FLOP count, longer step)")
+    ap.add_argument("--fuse-swiglu", type=int, default=1, choices=[0, 1],
+                    help="1: SwiGLU in the gate/up GEMM and down-dgrad GEMM epilogues; "
+                         "0: separate SwiGLU kernels")
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the headline step, print the sequence / GEMM-shape sweeps "
                          "(one JSON line each)")
@@ -244,7 +247,7 @@ def main():
     print(f"[bench] workload {w.name}: generating inputs", file=sys.stderr, flush=True)
     full = args.layer == "full"
     norm = norm_inputs(w, "qwen" if w.name.startswith("qwen") else "llama") if full else None
-    L = DecoderLayer(w, layer_inputs(w), norm=norm)
+    L = DecoderLayer(w, layer_inputs(w), norm=norm, fuse_swiglu=bool(args.fuse_swiglu))
     stream = torch.cuda.current_stream()
     fl = layer_flops(w)
 
@@ -316,9 +319,13 @@ def main():
         "attn_fwd_ms": round(avg["attn_fwd"], 4), "attn_fwd_tflops": round(attn_fwd_tflops, 1),
         "attn_bwd_ms": round(avg["attn_bwd"], 4), "attn_bwd_tflops": round(attn_bwd_tflops, 1),
         "attn_bwd_frac_peak": round(attn_bwd_tflops / PEAK_FP16_TFLOPS, 4),
-        "swiglu_fwd_ms": round(avg["swiglu_fwd"], 4), "swiglu_bwd_ms": round(avg["swiglu_bwd"], 4),
-        "swiglu_fwd_gbs": round(6 * w.T * w.F / (avg["swiglu_fwd"] * 1e-3) / 1e9, 1),
-        "swiglu_bwd_gbs": round(10 * w.T * w.F / (avg["swiglu_bwd"] * 1e-3) / 1e9, 1),
+        "swiglu": "fused into the gate/up and down-dgrad GEMM epilogues" if L.fuse_swiglu else
+                  "separate kernels",
+        **({} if L.fuse_swiglu else {
+            "swiglu_fwd_ms": round(avg["swiglu_fwd"], 4),
+            "swiglu_bwd_ms": round(avg["swiglu_bwd"], 4),
+            "swiglu_fwd_gbs": round(6 * w.T * w.F / (avg["swiglu_fwd"] * 1e-3) / 1e9, 1),
+            "swiglu_bwd_gbs": round(10 * w.T * w.F / (avg["swiglu_bwd"] * 1e-3) / 1e9, 1)}),
         "step_ms_median": round(float(np.median(step_ms)), 4),
         "step_ms_min": round(float(np.min(step_ms)), 4),
         "step_ms_max": round(float(np.max(step_ms)), 4),

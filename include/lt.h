@@ -187,6 +187,36 @@ lt_status lt_swiglu_bwd(const lt_half* dA, const lt_half* GU, lt_half* dGU,
                         int64_t T, int64_t F, lt_stream stream);
 
 /*
+ * Gate/up projection with the SwiGLU gate in its epilogue (the FFN
+ * projection of Sec. 4.1 followed by the evaluated models' gate, fused):
+ *   GU = X Wgu^T   (X [T, H], Wgu [2F, H]: gate rows 0..F-1, then up rows;
+ *                   GU [T, 2F]: G in columns 0..F-1, U in F..2F-1)
+ *   A  = silu(G) * U   [T, F]
+ * G and U are rounded once from the FP32 accumulators and equal those of
+ * lt_gemm_f16(0, 1, T, 2F, H, 1, X, ldx, Wgu, ldw, 0, GU, ldgu) bit for bit;
+ * A is computed from the same FP32 values (not from the rounded G, U).
+ * T, H, F multiples of 8, strides multiples of 8, pointers 16-byte aligned,
+ * 2*F*ldw < 2^30 - 128 (else LT_ERR_UNSUPPORTED).  GU and A must not overlap X,
+ * Wgu or each other.
+ */
+lt_status lt_gemm_gu_swiglu_f16(const lt_half* X, int64_t ldx, const lt_half* Wgu,
+                                int64_t ldw, lt_half* GU, int64_t ldgu, lt_half* A,
+                                int64_t lda, int64_t T, int64_t H, int64_t F,
+                                lt_stream stream);
+
+/*
+ * Down-projection data gradient with the SwiGLU backward in its epilogue:
+ *   dA  = dY Wd   (dY [T, H], Wd [H, F]; FP32, never stored)
+ *   dGU = [dA * U * s * (1 + G (1 - s)),  dA * silu(G)],  s = sigmoid(G),
+ * G and U read from GU [T, 2F]; dGU [T, 2F] is written once per element.
+ * Limits as lt_gemm_gu_swiglu_f16; dGU must not overlap the inputs.
+ */
+lt_status lt_gemm_swiglu_bwd_f16(const lt_half* dY, int64_t lddy, const lt_half* Wd,
+                                 int64_t ldwd, const lt_half* GU, int64_t ldgu,
+                                 lt_half* dGU, int64_t lddgu, int64_t T, int64_t H,
+                                 int64_t F, lt_stream stream);
+
+/*
  * RMSNorm of the evaluated models' decoder layers (Sec. 6.1 names LLaMA-2,
  * Baichuan2 and Qwen2.5; the paper itself defines no normalisation), per
  * token row x of width H:  r = (mean_j x_j^2 + eps)^(-1/2),  y = w * x * r.

@@ -46,7 +46,7 @@ namespace {
 //       16-lane group, groups 8 k-rows apart) then hit every bank once.
 // Both are filled by direct global -> LDS loads issued as opaque
 // instructions, so the caller orders them with explicit vmcnt waits.
-template <int R, int BK, bool KC, int NT>
+template <int R, int BK, bool KC, int NT, bool PAIRED = false>
 struct Operand {
   static constexpr int BYTES = R * BK * 2;
   static constexpr int NINST = BYTES / 1024;        // 1 KiB direct loads per slice
@@ -69,12 +69,27 @@ struct Operand {
   int64_t ld, row0;
   uint32_t nrec;
 
+  // PAIRED (K-contiguous only): tile row r = 32*blk + w reads matrix row
+  // row0 + 32*(blk/2) + w, plus pair_off for odd blk: alternating 32-row
+  // blocks of two row ranges (gate and up rows of a fused projection);
+  // `rows` bounds the index inside each range.
   __device__ __forceinline__ void init(const lt_half* b, int64_t ld_, int64_t row0_, int64_t rows,
-                                       int wave, int lane) {
+                                       int wave, int lane, int64_t pair_off = 0) {
     base = b;
     ld = ld_;
     row0 = row0_;
-    if constexpr (KC) {
+    if constexpr (PAIRED) {
+      static_assert(KC, "paired rows are K-contiguous");
+      nrec = 0x7fffffff;
+#pragma unroll
+      for (int t = 0; t < PERW; ++t) {
+        const int r = (wave * PERW + t) * RPI + lane / CPR;
+        const int64_t idx = row0 + 32 * (r >> 6) + (r & 31);
+        const int64_t abs_row = idx + ((r >> 5) & 1 ? pair_off : 0);
+        const int c = (lane % CPR) ^ swz(r);
+        voff[t] = idx < rows ? (uint32_t)((abs_row * ld + c * 8) * 2) : kOOB;
+      }
+    } else if constexpr (KC) {
       // rows past the matrix fall outside the buffer and read as zero
       const int64_t nvalid = rows - row0 < R ? rows - row0 : R;
       nrec = (uint32_t)(nvalid * ld * 2);
@@ -100,9 +115,10 @@ struct Operand {
   __device__ __forceinline__ void load(char* lds, int64_t k0, int kvalid, int wave, int lane) const {
     if constexpr (KC) {
       // descriptor based at column k0 of row row0: the range shrinks by the
-      // same 2*k0 bytes, so rows past the matrix still read as zero
-      const lt_half* b = base + row0 * ld + k0;
-      const uint32_t n = nrec - (uint32_t)(k0 * 2);
+      // same 2*k0 bytes, so rows past the matrix still read as zero (paired
+      // rows carry absolute offsets and explicit out-of-range offsets)
+      const lt_half* b = PAIRED ? base + k0 : base + row0 * ld + k0;
+      const uint32_t n = PAIRED ? nrec : nrec - (uint32_t)(k0 * 2);
 #pragma unroll
       for (int t = 0; t < PERW; ++t) {
         const int i = wave * PERW + t;
@@ -166,18 +182,21 @@ __device__ __forceinline__ void wait_slices(int n) {
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, int BK, int NS, bool TA, bool TB>
+__device__ __forceinline__ float sigmoid_f(float x) { return 1.f / (1.f + __expf(-x)); }
+
+template <int BM, int BN, int WGM, int WGN, int BK, int NS, bool TA, bool TB, int EPI>
 __global__ void __launch_bounds__(WGM * WGN * kWave)
 gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
                 const lt_half* __restrict__ A, int64_t lda,
                 const lt_half* __restrict__ B, int64_t ldb, float beta,
                 const lt_half* R, int64_t ldr, lt_half* C, int64_t ldc, int tiles_m,
-                int tiles_n, int group_m) {
+                int tiles_n, int group_m, lt_half* X1, int64_t ldx1, int64_t F) {
   constexpr int NT = WGM * WGN * kWave;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;   // wave tile
   constexpr int TM = WTM / 16, TN = WTN / 16;     // 16x16 MFMA blocks per wave
+  static_assert(EPI != 1 || (TB && WTN == 64), "paired gate/up tiles: 32 + 32 columns per wave");
   using OA = Operand<BM, BK, !TA, NT>;
-  using OB = Operand<BN, BK, TB, NT>;
+  using OB = Operand<BN, BK, TB, NT, EPI == 1>;
   constexpr int STAGE = OA::BYTES + OB::BYTES;
   constexpr int PER_SLICE = OA::PERW + OB::PERW;  // direct loads per wave per slice
   static_assert(NS >= 2 && (NS - 1) * PER_SLICE <= 63, "vmcnt range");
@@ -203,12 +222,16 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   const int gm = min(tiles_m - first_m, group_m);
   const int in_group = pid % group_size;
   const int64_t m0 = (int64_t)(first_m + in_group % gm) * BM;
-  const int64_t n0 = (int64_t)(in_group / gm) * BN;
+  // EPI 1: a tile covers BN/2 gate columns and the same BN/2 up columns
+  const int64_t n0 = (int64_t)(in_group / gm) * (EPI == 1 ? BN / 2 : BN);
 
   OA oa;
   OB ob;
   oa.init(A, lda, m0, M, wave, lane);
-  ob.init(B, ldb, n0, N, wave, lane);
+  if constexpr (EPI == 1)
+    ob.init(B, ldb, n0, F, wave, lane, F);
+  else
+    ob.init(B, ldb, n0, N, wave, lane);
 
   f32x4 acc[TM][TN];
 #pragma unroll
@@ -315,58 +338,156 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
     });
   }
 
-  // ---- epilogue: C[m][n..n+3] = alpha * acc + beta * R[m][n..n+3] ----
+  // ---- epilogue ----
   // lane holds column m = ... + lane % 16 and rows n = ... + 4*(lane/16) + 0..3
+  if constexpr (EPI == 1) {
+    // accumulator blocks j and j + TN/2 hold the gate and up columns of the
+    // same n: GU[m][n] = G, GU[m][F + n] = U, A[m][n] = silu(G) U (from the
+    // FP32 values, one rounding each)
 #pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    const int64_t m = m0 + wm * WTM + i * 16 + (lane & 15);
-    if (m >= M) continue;
+    for (int i = 0; i < TM; ++i) {
+      const int64_t m = m0 + wm * WTM + i * 16 + (lane & 15);
+      if (m >= M) continue;
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int64_t n = n0 + wn * WTN + j * 16 + 4 * (lane >> 4);
-      if (n >= N) continue;
-      float v[4];
+      for (int j = 0; j < TN / 2; ++j) {
+        const int64_t n = n0 + wn * (WTN / 2) + j * 16 + 4 * (lane >> 4);
+        if (n >= F) continue;
+        half4 g4, u4, a4;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = alpha * acc[i][j][e];
-      if (beta != 0.f) {
-        const half4 c = *reinterpret_cast<const half4*>(R + m * ldr + n);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] += beta * (float)c[e];
+        for (int e = 0; e < 4; ++e) {
+          const float g = alpha * acc[i][j][e];
+          const float u = alpha * acc[i][j + TN / 2][e];
+          g4[e] = (_Float16)g;
+          u4[e] = (_Float16)u;
+          a4[e] = (_Float16)(g * sigmoid_f(g) * u);
+        }
+        *reinterpret_cast<half4*>(C + m * ldc + n) = g4;
+        *reinterpret_cast<half4*>(C + m * ldc + F + n) = u4;
+        *reinterpret_cast<half4*>(X1 + m * ldx1 + n) = a4;
       }
-      half4 o;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) o[e] = (_Float16)v[e];
-      *reinterpret_cast<half4*>(C + m * ldc + n) = o;
     }
+  } else {
+    // The rows of the wave tile are handled in NG groups: the loads of group
+    // g (beta * R, or G and U for the SwiGLU gradient) are issued before the
+    // stores of group g - 1, and group g's values are computed only after
+    // those stores are in flight.  Loads and stores share one completion
+    // counter, so a load consumed after a store is waited for together with
+    // that store: in this order every group costs one overlapped memory
+    // round trip instead of one per 16x16 block.  R may be C itself; groups
+    // touch disjoint rows, so loading group g before storing group g - 1 is
+    // safe.
+    constexpr int NL = EPI == 2 ? 2 : 1;               // half4 per block and lane, in and out
+    constexpr int NG = EPI == 2 ? (TM >= 4 ? 4 : TM) : (TM >= 2 ? 2 : 1);
+    constexpr int IG = TM / NG;                        // accumulator rows per group
+    static_assert(TM % NG == 0, "row groups");
+    const bool reads = EPI == 2 || beta != 0.f;        // uniform over the grid
+    const int64_t mb = m0 + wm * WTM + (lane & 15);
+    const int64_t nb = n0 + wn * WTN + 4 * (lane >> 4);
+    half4 in[IG][TN][NL];
+    half4 out[IG][TN][NL];
+
+    // loads are unconditional, from addresses clamped into the matrix
+    // (values of out-of-range blocks are never stored): no branch between
+    // the loads keeps the completion-counter waits exact
+    auto load_group = [&](int g) {
+#pragma unroll
+      for (int ii = 0; ii < IG; ++ii) {
+        const int64_t m = mb + (g * IG + ii) * 16;
+        const int64_t mc = m < M ? m : M - 1;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int64_t n = nb + j * 16;
+          const int64_t nc = n < N ? n : N - 4;
+          if constexpr (EPI == 2) {
+            in[ii][j][0] = *reinterpret_cast<const half4*>(X1 + mc * ldx1 + nc);
+            in[ii][j][1] = *reinterpret_cast<const half4*>(X1 + mc * ldx1 + F + nc);
+          } else {
+            in[ii][j][0] = *reinterpret_cast<const half4*>(R + mc * ldr + nc);
+          }
+        }
+      }
+    };
+    auto compute_group = [&](int g) {
+#pragma unroll
+      for (int ii = 0; ii < IG; ++ii)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int i = g * IG + ii;
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = alpha * acc[i][j][e];
+          if constexpr (EPI == 2) {
+            // v = dA; dG = dA U s (1 + G (1 - s)),  dU = dA silu(G),  s = sigmoid(G)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float gv = (float)in[ii][j][0][e], uv = (float)in[ii][j][1][e];
+              const float sg = sigmoid_f(gv);
+              out[ii][j][0][e] = (_Float16)(v[e] * uv * sg * (1.f + gv * (1.f - sg)));
+              out[ii][j][1][e] = (_Float16)(v[e] * gv * sg);
+            }
+          } else {
+            if (reads) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] += beta * (float)in[ii][j][0][e];
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) out[ii][j][0][e] = (_Float16)v[e];
+          }
+        }
+    };
+    auto store_group = [&](int g) {
+#pragma unroll
+      for (int ii = 0; ii < IG; ++ii) {
+        const int64_t m = mb + (g * IG + ii) * 16;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int64_t n = nb + j * 16;
+          if (m < M && n < N) {
+            *reinterpret_cast<half4*>(C + m * ldc + n) = out[ii][j][0];
+            if constexpr (EPI == 2) *reinterpret_cast<half4*>(C + m * ldc + F + n) = out[ii][j][1];
+          }
+        }
+      }
+    };
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      if (reads) load_group(g);
+      if (g > 0) store_group(g - 1);
+      compute_group(g);
+    }
+    store_group(NG - 1);
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, int BK, int NS, bool TA, bool TB>
+template <int BM, int BN, int WGM, int WGN, int BK, int NS, bool TA, bool TB, int EPI>
 hipError_t launch(const GemmArgs& g, hipStream_t s) {
   const int tiles_m = (int)((g.M + BM - 1) / BM);
-  const int tiles_n = (int)((g.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_f16_kernel<BM, BN, WGM, WGN, BK, NS, TA, TB>), dim3(tiles_m * tiles_n),
-                     dim3(WGM * WGN * kWave), 0, s, g.M, g.N, g.K, g.alpha, g.A, g.lda, g.B, g.ldb,
-                     g.beta, g.R, g.ldr, g.C, g.ldc, tiles_m, tiles_n, 8);
+  const int tiles_n = EPI == 1 ? (int)((g.F + BN / 2 - 1) / (BN / 2)) : (int)((g.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_f16_kernel<BM, BN, WGM, WGN, BK, NS, TA, TB, EPI>),
+                     dim3(tiles_m * tiles_n), dim3(WGM * WGN * kWave), 0, s, g.M, g.N, g.K, g.alpha,
+                     g.A, g.lda, g.B, g.ldb, g.beta, g.R, g.ldr, g.C, g.ldc, tiles_m, tiles_n, 8,
+                     g.X1, g.ldx1, g.F);
   return hipGetLastError();
 }
 
-template <bool TA, bool TB>
+template <bool TA, bool TB, int EPI>
 hipError_t dispatch_tile(const GemmArgs& g, hipStream_t s) {
   // 256x256 tiles once there are about as many tiles as CUs; smaller
   // problems use 128x128 tiles so that more workgroups exist.
   const int64_t big_tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
-  if (big_tiles >= 192) return launch<256, 256, 2, 4, 64, 2, TA, TB>(g, s);
-  return launch<128, 128, 2, 2, 64, 2, TA, TB>(g, s);
+  if (big_tiles >= 192) return launch<256, 256, 2, 4, 64, 2, TA, TB, EPI>(g, s);
+  return launch<128, 128, 2, 2, 64, 2, TA, TB, EPI>(g, s);
 }
 
 }  // namespace
 
 hipError_t gemm_f16_launch(const GemmArgs& g, hipStream_t s) {
+  if (g.epi == 1) return dispatch_tile<false, true, 1>(g, s);     // X Wgu^T
+  if (g.epi == 2) return dispatch_tile<false, false, 2>(g, s);    // dY Wd
   if (g.transA) {
-    return g.transB ? dispatch_tile<true, true>(g, s) : dispatch_tile<true, false>(g, s);
+    return g.transB ? dispatch_tile<true, true, 0>(g, s) : dispatch_tile<true, false, 0>(g, s);
   }
-  return g.transB ? dispatch_tile<false, true>(g, s) : dispatch_tile<false, false>(g, s);
+  return g.transB ? dispatch_tile<false, true, 0>(g, s) : dispatch_tile<false, false, 0>(g, s);
 }
 
 }  // namespace lt

@@ -22,6 +22,14 @@ struct GemmArgs {
   int64_t ldr;
   lt_half* C;
   int64_t ldc;
+  // fused SwiGLU epilogues (0: none)
+  //   1: B = Wgu [2F, K] (gate rows, then up rows), C = GU [M, 2F]; each tile
+  //      pairs gate and up columns and also writes X1 = A = silu(G) * U [M, F]
+  //   2: C = dGU [M, 2F] from dA = op(A) op(B) [M, F = N] and X1 = GU [M, 2F]
+  int epi = 0;
+  lt_half* X1 = nullptr;
+  int64_t ldx1 = 0;
+  int64_t F = 0;
 };
 
 struct AttnShape {

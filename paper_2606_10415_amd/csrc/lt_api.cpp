@@ -177,6 +177,58 @@ lt_status lt_attn_bwd(const lt_half* Q, const lt_half* K, const lt_half* V, int6
   return from_hip(lt::attn_bwd_launch(a, reinterpret_cast<hipStream_t>(stream)), "attn_bwd launch");
 }
 
+lt_status lt_gemm_gu_swiglu_f16(const lt_half* X, int64_t ldx, const lt_half* Wgu, int64_t ldw,
+                                lt_half* GU, int64_t ldgu, lt_half* A, int64_t lda, int64_t T,
+                                int64_t H, int64_t F, lt_stream stream) {
+  if (T < 0 || H < 0 || F < 0) return fail(LT_ERR_INVALID_ARG, "negative size");
+  if (T == 0 || F == 0) return ok();
+  if (!X || !Wgu || !GU || !A) return fail(LT_ERR_INVALID_ARG, "NULL pointer");
+  if (ldx < H || ldw < H || ldgu < 2 * F || lda < F)
+    return fail(LT_ERR_INVALID_ARG, "row stride smaller than the row length");
+  if ((T | H | F) & 7) return fail(LT_ERR_UNSUPPORTED, "T, H, F must be multiples of 8");
+  if ((ldx | ldw | ldgu | lda) & 7)
+    return fail(LT_ERR_UNSUPPORTED, "leading dimensions must be multiples of 8");
+  if (!aligned16(X) || !aligned16(Wgu) || !aligned16(GU) || !aligned16(A))
+    return fail(LT_ERR_UNSUPPORTED, "X, Wgu, GU, A must be 16-byte aligned");
+  if (T > (int64_t)1 << 30 || F > (int64_t)1 << 29 || H > (int64_t)1 << 30)
+    return fail(LT_ERR_UNSUPPORTED, "T, H or F too large for the tile grid");
+  if (ldx >= ((int64_t)1 << 22) || ldw >= ((int64_t)1 << 22) || 2 * F * ldw >= ((int64_t)1 << 30) - 128)
+    return fail(LT_ERR_UNSUPPORTED, "operands too large for 32-bit buffer offsets");
+  lt::GemmArgs g{0, 1, T, 2 * F, H, 1.f, 0.f, X, ldx, Wgu, ldw, GU, ldgu, GU, ldgu};
+  g.epi = 1;
+  g.X1 = A;
+  g.ldx1 = lda;
+  g.F = F;
+  return from_hip(lt::gemm_f16_launch(g, reinterpret_cast<hipStream_t>(stream)),
+                  "gemm_gu_swiglu launch");
+}
+
+lt_status lt_gemm_swiglu_bwd_f16(const lt_half* dY, int64_t lddy, const lt_half* Wd, int64_t ldwd,
+                                 const lt_half* GU, int64_t ldgu, lt_half* dGU, int64_t lddgu,
+                                 int64_t T, int64_t H, int64_t F, lt_stream stream) {
+  if (T < 0 || H < 0 || F < 0) return fail(LT_ERR_INVALID_ARG, "negative size");
+  if (T == 0 || F == 0) return ok();
+  if (!dY || !Wd || !GU || !dGU) return fail(LT_ERR_INVALID_ARG, "NULL pointer");
+  if (lddy < H || ldwd < F || ldgu < 2 * F || lddgu < 2 * F)
+    return fail(LT_ERR_INVALID_ARG, "row stride smaller than the row length");
+  if ((T | H | F) & 7) return fail(LT_ERR_UNSUPPORTED, "T, H, F must be multiples of 8");
+  if ((lddy | ldwd | ldgu | lddgu) & 7)
+    return fail(LT_ERR_UNSUPPORTED, "leading dimensions must be multiples of 8");
+  if (!aligned16(dY) || !aligned16(Wd) || !aligned16(GU) || !aligned16(dGU))
+    return fail(LT_ERR_UNSUPPORTED, "dY, Wd, GU, dGU must be 16-byte aligned");
+  if (T > (int64_t)1 << 30 || F > (int64_t)1 << 30 || H > (int64_t)1 << 30)
+    return fail(LT_ERR_UNSUPPORTED, "T, H or F too large for the tile grid");
+  if (lddy >= ((int64_t)1 << 22) || ldwd >= ((int64_t)1 << 22))
+    return fail(LT_ERR_UNSUPPORTED, "lddy/ldwd must be < 2^22 elements (32-bit buffer offsets)");
+  lt::GemmArgs g{0, 0, T, F, H, 1.f, 0.f, dY, lddy, Wd, ldwd, dGU, lddgu, dGU, lddgu};
+  g.epi = 2;
+  g.X1 = const_cast<lt_half*>(GU);
+  g.ldx1 = ldgu;
+  g.F = F;
+  return from_hip(lt::gemm_f16_launch(g, reinterpret_cast<hipStream_t>(stream)),
+                  "gemm_swiglu_bwd launch");
+}
+
 size_t lt_rmsnorm_bwd_workspace_size(int64_t T, int64_t H) {
   if (T < 1 || H < 1) return 0;
   return lt::rmsnorm_bwd_ws_bytes(T, H);

@@ -16,6 +16,10 @@ are RMSNorm-ed before the QKV and gate/up projections (Xn, H1n), Q and K are
 rotated in place in QKV, and the backward runs the inverse rotation on dQ, dK
 and RMSNorm backward (with the residual gradient added in the same pass):
     dH1 = dY + rmsnorm_bwd(dGU Wgu) ;  dX = dH1 + rmsnorm_bwd(dQKV Wqkv)
+
+With ``fuse_swiglu`` the SwiGLU gate runs in the epilogues of the gate/up
+GEMM (A from the FP32 accumulators, GU still stored for the backward) and of
+the down-projection dgrad (dGU written directly, dA never stored).
 """
 
 import math
@@ -31,10 +35,12 @@ class DecoderLayer:
     ``shape`` needs attributes B, S, H, Hq, Hkv, D, F.  ``params`` maps
     X, dY, Wqkv, Wo, Wgu, Wd to float16 tensors (host or device).  ``norm``
     (optional) has attributes wn1, wn2 (RMSNorm weights [H]), eps, rope_base.
+    ``fuse_swiglu`` selects the GEMMs with the SwiGLU epilogues.
     """
 
-    def __init__(self, shape, params, device="cuda", norm=None):
+    def __init__(self, shape, params, device="cuda", norm=None, fuse_swiglu=True):
         self.sh = sh = shape
+        self.fuse_swiglu = bool(fuse_swiglu)
         self.dev = torch.device(device)
         T = sh.B * sh.S
         self.T = T
@@ -127,11 +133,16 @@ class DecoderLayer:
                               self.eps, stream)
             mark("rmsnorm2_fwd")
             hin = self.H1n
-        lt.lt_gemm_f16(0, 1, T, 2 * sh.F, sh.H, 1.0, hin, sh.H, self.Wgu, sh.H, 0.0, self.GU,
-                       2 * sh.F, stream)
-        mark("gu_fwd")
-        lt.lt_swiglu_fwd(self.GU, self.A, T, sh.F, stream)
-        mark("swiglu_fwd")
+        if self.fuse_swiglu:
+            lt.lt_gemm_gu_swiglu_f16(hin, sh.H, self.Wgu, sh.H, self.GU, 2 * sh.F, self.A, sh.F, T,
+                                     sh.H, sh.F, stream)
+            mark("gu_fwd")
+        else:
+            lt.lt_gemm_f16(0, 1, T, 2 * sh.F, sh.H, 1.0, hin, sh.H, self.Wgu, sh.H, 0.0, self.GU,
+                           2 * sh.F, stream)
+            mark("gu_fwd")
+            lt.lt_swiglu_fwd(self.GU, self.A, T, sh.F, stream)
+            mark("swiglu_fwd")
         lt.lt_gemm_f16_res(0, 1, T, sh.H, sh.F, 1.0, self.A, sh.F, self.Wd, sh.F, 1.0, self.H1,
                            sh.H, self.Y, sh.H, stream)
         mark("down_fwd")
@@ -143,11 +154,16 @@ class DecoderLayer:
         lt.lt_gemm_f16(1, 0, sh.H, sh.F, T, 1.0, self.dY, sh.H, self.A, sh.F, 0.0, self.dWd, sh.F,
                        stream)
         mark("down_wgrad")
-        lt.lt_gemm_f16(0, 0, T, sh.F, sh.H, 1.0, self.dY, sh.H, self.Wd, sh.F, 0.0, self.dA, sh.F,
-                       stream)
-        mark("down_dgrad")
-        lt.lt_swiglu_bwd(self.dA, self.GU, self.dGU, T, sh.F, stream)
-        mark("swiglu_bwd")
+        if self.fuse_swiglu:
+            lt.lt_gemm_swiglu_bwd_f16(self.dY, sh.H, self.Wd, sh.F, self.GU, 2 * sh.F, self.dGU,
+                                      2 * sh.F, T, sh.H, sh.F, stream)
+            mark("down_dgrad")
+        else:
+            lt.lt_gemm_f16(0, 0, T, sh.F, sh.H, 1.0, self.dY, sh.H, self.Wd, sh.F, 0.0, self.dA,
+                           sh.F, stream)
+            mark("down_dgrad")
+            lt.lt_swiglu_bwd(self.dA, self.GU, self.dGU, T, sh.F, stream)
+            mark("swiglu_bwd")
         # gate/up projection
         hin = self.H1n if self.norm is not None else self.H1
         lt.lt_gemm_f16(1, 0, 2 * sh.F, sh.H, T, 1.0, self.dGU, 2 * sh.F, hin, sh.H, 0.0,

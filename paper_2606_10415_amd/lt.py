@@ -86,6 +86,11 @@ _lib.lt_swiglu_fwd.restype = _int
 _lib.lt_swiglu_fwd.argtypes = [_vp, _vp, _i64, _i64, _vp]
 _lib.lt_swiglu_bwd.restype = _int
 _lib.lt_swiglu_bwd.argtypes = [_vp, _vp, _vp, _i64, _i64, _vp]
+_lib.lt_gemm_gu_swiglu_f16.restype = _int
+_lib.lt_gemm_gu_swiglu_f16.argtypes = [_vp, _i64, _vp, _i64, _vp, _i64, _vp, _i64, _i64, _i64, _i64, _vp]
+_lib.lt_gemm_swiglu_bwd_f16.restype = _int
+_lib.lt_gemm_swiglu_bwd_f16.argtypes = [_vp, _i64, _vp, _i64, _vp, _i64, _vp, _i64, _i64, _i64, _i64,
+                                        _vp]
 _lib.lt_rmsnorm_fwd.restype = _int
 _lib.lt_rmsnorm_fwd.argtypes = [_vp, _i64, _vp, _vp, _i64, _vp, _i64, _i64, _f32, _vp]
 _lib.lt_rmsnorm_bwd_workspace_size.restype = _sz
@@ -178,6 +183,18 @@ def lt_swiglu_fwd(GU, A, T, F, stream=None):
 def lt_swiglu_bwd(dA, GU, dGU, T, F, stream=None):
     _check(_lib.lt_swiglu_bwd(_ptr(dA), _ptr(GU), _ptr(dGU), int(T), int(F), _stream(stream)),
            "lt_swiglu_bwd")
+
+
+def lt_gemm_gu_swiglu_f16(X, ldx, Wgu, ldw, GU, ldgu, A, lda, T, H, F, stream=None):
+    _check(_lib.lt_gemm_gu_swiglu_f16(_ptr(X), int(ldx), _ptr(Wgu), int(ldw), _ptr(GU), int(ldgu),
+                                      _ptr(A), int(lda), int(T), int(H), int(F), _stream(stream)),
+           "lt_gemm_gu_swiglu_f16")
+
+
+def lt_gemm_swiglu_bwd_f16(dY, lddy, Wd, ldwd, GU, ldgu, dGU, lddgu, T, H, F, stream=None):
+    _check(_lib.lt_gemm_swiglu_bwd_f16(_ptr(dY), int(lddy), _ptr(Wd), int(ldwd), _ptr(GU),
+                                       int(ldgu), _ptr(dGU), int(lddgu), int(T), int(H), int(F),
+                                       _stream(stream)), "lt_gemm_swiglu_bwd_f16")
 
 
 def lt_rmsnorm_fwd(X, ldx, W, Y, ldy, RSTD, T, H, eps, stream=None):

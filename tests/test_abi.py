@@ -15,7 +15,7 @@ def test_every_declared_symbol_is_exported():
             "lt_attn_bwd_workspace_size", "lt_swiglu_fwd", "lt_swiglu_bwd",
             "lt_status_string", "lt_last_error", "lt_version", "lt_rmsnorm_fwd",
             "lt_rmsnorm_bwd", "lt_rmsnorm_bwd_workspace_size", "lt_rope_table",
-            "lt_rope_f16"} <= set(names)
+            "lt_rope_f16", "lt_gemm_gu_swiglu_f16", "lt_gemm_swiglu_bwd_f16"} <= set(names)
     for n in names:
         assert hasattr(lt._lib, n), f"{n} declared in lt.h but not exported"
 
@@ -205,3 +205,48 @@ def test_rope_rejects_on_host(kw, status):
     st = lt._lib.lt_rope_f16(a["X"], a["stride"], a["B"], a["S"], a["heads"], a["D"], a["CS"],
                              a["inverse"], None)
     assert st == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(T=-8), lt.LT_ERR_INVALID_ARG),
+    (dict(X=None), lt.LT_ERR_INVALID_ARG),
+    (dict(A=None), lt.LT_ERR_INVALID_ARG),
+    (dict(ldgu=1000), lt.LT_ERR_INVALID_ARG),         # below 2F
+    (dict(lda=600), lt.LT_ERR_INVALID_ARG),           # below F
+    (dict(ldx=100), lt.LT_ERR_INVALID_ARG),           # below H
+    (dict(T=12), lt.LT_ERR_UNSUPPORTED),
+    (dict(F=684, ldgu=1368, lda=684), lt.LT_ERR_UNSUPPORTED),
+    (dict(ldw=132), lt.LT_ERR_UNSUPPORTED),
+    (dict(GU=FAKE + 2), lt.LT_ERR_UNSUPPORTED),
+])
+def test_gemm_gu_swiglu_rejects_on_host(kw, status):
+    a = dict(X=FAKE, ldx=128, Wgu=FAKE, ldw=128, GU=FAKE, ldgu=1376, A=FAKE, lda=688, T=64,
+             H=128, F=688)
+    a.update(kw)
+    st = lt._lib.lt_gemm_gu_swiglu_f16(a["X"], a["ldx"], a["Wgu"], a["ldw"], a["GU"], a["ldgu"],
+                                       a["A"], a["lda"], a["T"], a["H"], a["F"], None)
+    assert st == status
+    assert lt.last_error() != ""
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(F=-8), lt.LT_ERR_INVALID_ARG),
+    (dict(GU=None), lt.LT_ERR_INVALID_ARG),
+    (dict(ldwd=600), lt.LT_ERR_INVALID_ARG),          # below F
+    (dict(lddgu=1000), lt.LT_ERR_INVALID_ARG),        # below 2F
+    (dict(H=60, lddy=60), lt.LT_ERR_UNSUPPORTED),
+    (dict(dGU=FAKE + 4), lt.LT_ERR_UNSUPPORTED),
+])
+def test_gemm_swiglu_bwd_rejects_on_host(kw, status):
+    a = dict(dY=FAKE, lddy=128, Wd=FAKE, ldwd=688, GU=FAKE, ldgu=1376, dGU=FAKE, lddgu=1376,
+             T=64, H=128, F=688)
+    a.update(kw)
+    st = lt._lib.lt_gemm_swiglu_bwd_f16(a["dY"], a["lddy"], a["Wd"], a["ldwd"], a["GU"],
+                                        a["ldgu"], a["dGU"], a["lddgu"], a["T"], a["H"], a["F"],
+                                        None)
+    assert st == status
+
+
+def test_fused_swiglu_empty_is_noop():
+    assert lt._lib.lt_gemm_gu_swiglu_f16(None, 8, None, 8, None, 0, None, 0, 0, 8, 8, None) == lt.LT_OK
+    assert lt._lib.lt_gemm_swiglu_bwd_f16(None, 8, None, 8, None, 0, None, 0, 8, 8, 0, None) == lt.LT_OK

@@ -93,14 +93,15 @@ def test_rope_parity(env, B, S, Hq, Hkv, D, base):
                                       (Workload("tiny-gqa", 10, B=2, S=136, H=256, Hq=4, Hkv=2,
                                                 D=64, F=344), "qwen")],
                          ids=["tiny-llama", "tiny-gqa-ragged-qwen"])
-def test_full_layer_chained_parity(env, w, family):
+@pytest.mark.parametrize("fuse", [False, True], ids=["swiglu-kernels", "swiglu-fused"])
+def test_full_layer_chained_parity(env, w, family, fuse):
     """RMSNorm + rotary embedding + attention + SwiGLU MLP, fwd and bwd, chained."""
-    print(f"full layer chained {w.name} {family}", flush=True)
+    print(f"full layer chained {w.name} {family} fuse_swiglu={fuse}", flush=True)
     torch, lt = env
     from paper_2606_10415_amd.layer import DecoderLayer
     p = layer_inputs(w)
     n = norm_inputs(w, family)
-    L = DecoderLayer(w, p, norm=n)
+    L = DecoderLayer(w, p, norm=n, fuse_swiglu=fuse)
     L.step()
     torch.cuda.synchronize()
     sh = oracle.LayerShape(w.B, w.S, w.H, w.Hq, w.Hkv, w.D, w.F)

@@ -1,7 +1,10 @@
-"""GPU parity of the SwiGLU kernels and of the chained decoder layer.
+"""GPU parity of the SwiGLU kernels, the GEMMs with SwiGLU epilogues and of
+the chained decoder layer.
 
 Bars: SwiGLU outputs relative Frobenius error <= 5e-3 (per op, same fp16
-inputs); chained layer (one fp16 input set, the GPU keeps fp16
+inputs); the fused gate/up GEMM's GU bitwise equal to the plain GEMM's (same
+tiles, same reduction order) and its A, the fused down-dgrad's dGU <= 5e-3
+against the oracle (sampled rows at full size); chained layer (one fp16 input set, the GPU keeps fp16
 intermediates, the oracle keeps float64 throughout): Y, dX and the four
 weight gradients <= 5e-3, dQKV <= 1e-2.
 """
@@ -56,11 +59,42 @@ def test_swiglu_extreme_inputs(env):
     np.testing.assert_allclose(a, oracle.swiglu_fwd(gu), rtol=2e-3, atol=1e-6)
 
 
-def _chained(env, w):
+@pytest.mark.parametrize("T,H,F", [(272, 256, 344), (64, 128, 688), (8, 64, 8), (1000, 512, 1000),
+                                   (4096, 4096, 11008), (2048, 5120, 13824),
+                                   (2040, 512, 5000)])
+def test_fused_gemm_swiglu_parity(env, T, H, F):
+    print(f"fused gemm swiglu T={T} H={H} F={F}", flush=True)
+    torch, lt = env
+    x = normal_f16(61, (T, H))
+    wgu = normal_f16(62, (2 * F, H), 0.02)
+    dy = normal_f16(63, (T, H))
+    wd = normal_f16(64, (H, F), 0.02)
+    cu = lambda a: torch.from_numpy(a).cuda()
+    X, Wgu, dY, Wd = cu(x), cu(wgu), cu(dy), cu(wd)
+    e = lambda *s_: torch.full(s_, float("nan"), dtype=torch.float16, device="cuda")
+    GU, A, GUref, dGU = e(T, 2 * F), e(T, F), e(T, 2 * F), e(T, 2 * F)
+    lt.lt_gemm_gu_swiglu_f16(X, H, Wgu, H, GU, 2 * F, A, F, T, H, F)
+    lt.lt_gemm_f16(0, 1, T, 2 * F, H, 1.0, X, H, Wgu, H, 0.0, GUref, 2 * F)
+    lt.lt_gemm_swiglu_bwd_f16(dY, H, Wd, F, GU, 2 * F, dGU, 2 * F, T, H, F)
+    torch.cuda.synchronize()
+    assert torch.equal(GU.view(torch.int16), GUref.view(torch.int16))
+    rows = np.arange(T) if T <= 1024 else np.unique(
+        np.concatenate([np.random.default_rng(7).choice(T, 40, replace=False), [0, T - 1]]))
+    gu = GU.cpu().numpy()
+    gu_ref = oracle.gemm(0, 1, 1.0, x[rows], wgu)
+    err_gu = rel_f(gu[rows], gu_ref)
+    err_a = rel_f(A.cpu().numpy()[rows], oracle.swiglu_fwd(gu_ref))
+    da_ref = oracle.gemm(0, 0, 1.0, dy[rows], wd)
+    err_dgu = rel_f(dGU.cpu().numpy()[rows], oracle.swiglu_bwd(da_ref, gu[rows]))
+    print(f"  GU {err_gu:.3e}  A {err_a:.3e}  dGU {err_dgu:.3e}", flush=True)
+    assert err_gu <= 5e-3 and err_a <= 5e-3 and err_dgu <= 5e-3
+
+
+def _chained(env, w, fuse=False):
     torch, lt = env
     from paper_2606_10415_amd.layer import DecoderLayer
     p = layer_inputs(w)
-    L = DecoderLayer(w, p)
+    L = DecoderLayer(w, p, fuse_swiglu=fuse)
     L.step()
     torch.cuda.synchronize()
     return p, L
@@ -69,9 +103,10 @@ def _chained(env, w):
 @pytest.mark.parametrize("w", [WORKLOADS["tiny"],
                                Workload("tiny-gqa", 10, B=2, S=136, H=256, Hq=4, Hkv=2, D=64, F=344)],
                          ids=["tiny", "tiny-gqa-ragged"])
-def test_layer_chained_parity(env, w):
-    print(f"layer chained {w.name}", flush=True)
-    p, L = _chained(env, w)
+@pytest.mark.parametrize("fuse", [False, True], ids=["swiglu-kernels", "swiglu-fused"])
+def test_layer_chained_parity(env, w, fuse):
+    print(f"layer chained {w.name} fuse_swiglu={fuse}", flush=True)
+    p, L = _chained(env, w, fuse)
     sh = oracle.LayerShape(w.B, w.S, w.H, w.Hq, w.Hkv, w.D, w.F)
     acts = oracle.layer_fwd(sh, p["X"], p["Wqkv"], p["Wo"], p["Wgu"], p["Wd"])
     grads = oracle.layer_bwd(sh, p["X"], p["Wqkv"], p["Wo"], p["Wgu"], p["Wd"], p["dY"], acts)
