@@ -10,6 +10,7 @@ float64, from the float16 input values (the paper states that its backend
 preserves the model computation exactly; Sec. 4.1 and Sec. 5.3):
 
 * ``gemm``       -- C = alpha * op(A) @ op(B) + beta * C           (Sec. 4.1, FP16 GEMM backend)
+                    and the column sum that is a bias gradient
 * ``attention``  -- causal / GQA softmax attention forward and its
                     gradient (Sec. 4.1, Algorithm 1, Memory-resident
                     Attention Backward)
@@ -28,14 +29,14 @@ Every function here is pinned by the CPU tests in ``tests/test_oracle_*.py``
 worked examples under ``tests/golden/``).
 """
 
-from .gemm import gemm, gemm_entries
+from .gemm import gemm, gemm_entries, column_sum
 from .attention import attn_fwd, attn_bwd, attn_head_fwd, attn_head_bwd
 from .swiglu import silu, swiglu_fwd, swiglu_bwd
 from .norm_rope import rmsnorm_fwd, rmsnorm_bwd, rope_angles, rope_fwd, rope_bwd
 from .layer import LayerShape, LayerNorms, layer_fwd, layer_bwd, layer_flops
 
 __all__ = [
-    "gemm", "gemm_entries",
+    "gemm", "gemm_entries", "column_sum",
     "attn_fwd", "attn_bwd", "attn_head_fwd", "attn_head_bwd",
     "silu", "swiglu_fwd", "swiglu_bwd",
     "rmsnorm_fwd", "rmsnorm_bwd", "rope_angles", "rope_fwd", "rope_bwd",

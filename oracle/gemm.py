@@ -54,3 +54,9 @@ def gemm_entries(transA, transB, alpha, A, B, beta, C, rows, cols):
     if beta != 0.0:
         out = out + float(beta) * np.asarray(C, dtype=np.float64)[rows, cols]
     return out
+
+
+def column_sum(X):
+    """Sum over the rows of X [T, N] in float64: the gradient of a bias that is
+    broadcast over the T rows of a linear layer's output."""
+    return np.sum(np.asarray(X, dtype=np.float64), axis=0)

@@ -34,6 +34,12 @@ rotated (norm_rope.py):
 and the backward adds rmsnorm_bwd after each block's input GEMM gradient
 and the inverse rotation of dQ, dK before the QKV weight / data gradients.
 
+Qwen2.5's QKV projection carries a bias (``norm.bqkv``, [(Hq + 2 Hkv) d]): it
+is part of the linear layer, so it is added to QKV before the rotation, and
+its gradient is the column sum of dQKV taken after the inverse rotation:
+
+    QKV = Xn Wqkv^T + bqkv ;   dbqkv = sum over rows of dQKV
+
 All intermediates stay float64 (no float16 rounding of intermediates).
 """
 
@@ -42,6 +48,7 @@ from dataclasses import dataclass
 import numpy as np
 
 from .attention import attn_fwd, attn_bwd
+from .gemm import column_sum
 from .norm_rope import rmsnorm_fwd, rmsnorm_bwd, rope_fwd, rope_bwd
 from .swiglu import swiglu_fwd, swiglu_bwd
 
@@ -71,6 +78,7 @@ class LayerNorms:
     wn2: object          # RMSNorm weight of the FFN input [H]
     eps: float = 1e-5
     rope_base: float = 10000.0
+    bqkv: object = None  # QKV projection bias [(Hq + 2 Hkv) d] (Qwen2.5), or None
 
 
 def _split_qkv(qkv, sh):
@@ -94,6 +102,8 @@ def layer_fwd(sh, X, Wqkv, Wo, Wgu, Wd, norm=None):
         Xin, acts["rstd1"] = rmsnorm_fwd(X, norm.wn1, norm.eps)
         acts["Xn"] = Xin
     qkv = Xin @ Wqkv.T
+    if norm is not None and norm.bqkv is not None:
+        qkv = qkv + np.asarray(norm.bqkv, dtype=np.float64)[None, :]
     q, k, v = _split_qkv(qkv, sh)
     if norm is not None:
         q, k = rope_fwd(q, norm.rope_base), rope_fwd(k, norm.rope_base)
@@ -114,7 +124,8 @@ def layer_fwd(sh, X, Wqkv, Wo, Wgu, Wd, norm=None):
 
 def layer_bwd(sh, X, Wqkv, Wo, Wgu, Wd, dY, acts=None, norm=None):
     """Gradient of sum(Y * dY) w.r.t. X and the weights (float64 dict; with
-    ``norm`` also 'dWn1', 'dWn2' for the two RMSNorm weights)."""
+    ``norm`` also 'dWn1', 'dWn2' for the two RMSNorm weights, and 'dbqkv' when
+    the norm carries a QKV bias)."""
     X = np.asarray(X, dtype=np.float64)
     Wqkv, Wo, Wgu, Wd = (np.asarray(w, dtype=np.float64) for w in (Wqkv, Wo, Wgu, Wd))
     dY = np.asarray(dY, dtype=np.float64)
@@ -139,6 +150,8 @@ def layer_bwd(sh, X, Wqkv, Wo, Wgu, Wd, dY, acts=None, norm=None):
     if norm is not None:
         dq, dk = rope_bwd(dq, norm.rope_base), rope_bwd(dk, norm.rope_base)
     dQKV = np.concatenate([dq.reshape(sh.T, -1), dk.reshape(sh.T, -1), dv.reshape(sh.T, -1)], axis=1)
+    if norm is not None and norm.bqkv is not None:
+        out["dbqkv"] = column_sum(dQKV)
     dWqkv = dQKV.T @ (acts["Xn"] if norm is not None else X)
     dXin = dQKV @ Wqkv
     if norm is not None:

@@ -50,16 +50,18 @@ WORKLOADS = {
 }
 
 TENSOR_INDEX = {"X": 0, "dY": 1, "Wqkv": 2, "Wo": 3, "Wgu": 4, "Wd": 5,
-                "Q": 6, "K": 7, "V": 8, "dO": 9, "Wn1": 10, "Wn2": 11}
+                "Q": 6, "K": 7, "V": 8, "dO": 9, "Wn1": 10, "Wn2": 11, "bqkv": 12}
 
 
 @dataclass(frozen=True)
 class NormInputs:
-    """RMSNorm weights [H] of the attention and FFN inputs, eps and rotary base."""
+    """RMSNorm weights [H] of the attention and FFN inputs, eps, rotary base
+    and the QKV projection bias [(Hq + 2 Hkv) d] (Qwen2.5; None for LLaMA-2)."""
     wn1: np.ndarray
     wn2: np.ndarray
     eps: float
     rope_base: float
+    bqkv: object = None
 
 
 # eps and rotary base of the evaluated model families (their published
@@ -97,13 +99,15 @@ def layer_inputs(w):
 
 
 def norm_inputs(w, family="llama"):
-    """RMSNorm weights 1 + N(0, 0.1^2) (float16) for workload ``w`` and the
-    family's eps and rotary base."""
+    """RMSNorm weights 1 + N(0, 0.1^2) (float16) for workload ``w``, the
+    family's eps and rotary base, and for "qwen" a QKV bias N(0, 0.5^2)."""
     base = 1000 * w.index
     t = TENSOR_INDEX
     eps, rope_base = NORM_CONSTANTS[family]
     one = lambda seed: (1.0 + normal_f16(seed, (w.H,), 0.1).astype(np.float32)).astype(np.float16)
-    return NormInputs(one(base + t["Wn1"]), one(base + t["Wn2"]), eps, rope_base)
+    bqkv = (normal_f16(base + t["bqkv"], ((w.Hq + 2 * w.Hkv) * w.D,), 0.5) if family == "qwen"
+            else None)
+    return NormInputs(one(base + t["Wn1"]), one(base + t["Wn2"]), eps, rope_base, bqkv)
 
 
 def attention_inputs(B, S, Hq, Hkv, D, seed_base=0, qk_std=1.0):

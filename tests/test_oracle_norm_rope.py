@@ -7,16 +7,21 @@ Rotary embedding: position 0 is the identity; every (i, i + d/2) pair keeps
 its norm; scores depend only on the position difference; the backward is the
 inverse rotation and matches finite differences; a hand-derived worked
 example fixes the pairing and the signs.
-Full layer (RMSNorm + rotary embedding + attention + SwiGLU MLP): finite
-differences w.r.t. X, the four projection weights and both RMSNorm weights.
+Full layer (RMSNorm + rotary embedding + attention + SwiGLU MLP, with the
+Qwen2.5 QKV bias): finite differences w.r.t. X, the four projection weights,
+both RMSNorm weights and the QKV bias; with a zero QKV weight the attention
+output equals the V bias (attention averages identical values); with Q and K
+from the bias alone, the first off-diagonal score is the one the rotation of
+the biased Q at position 1 gives, which fixes the bias before the rotation.
+Column sum (the bias gradient): brute force over a small matrix.
 """
 
 import numpy as np
 import pytest
 
 from conftest import golden_value, load_golden, rel_f
-from oracle import (LayerNorms, LayerShape, layer_bwd, layer_fwd, rmsnorm_bwd, rmsnorm_fwd,
-                    rope_angles, rope_bwd, rope_fwd)
+from oracle import (LayerNorms, LayerShape, column_sum, layer_bwd, layer_fwd, rmsnorm_bwd,
+                    rmsnorm_fwd, rope_angles, rope_bwd, rope_fwd)
 
 
 def _fd_grad(f, x, h=1e-6):
@@ -150,18 +155,18 @@ def _full_params(seed):
          "Wd": 0.3 * rng.standard_normal((sh.H, sh.F)),
          "dY": rng.standard_normal((sh.T, sh.H))}
     norms = LayerNorms(wn1=1 + 0.2 * rng.standard_normal(sh.H), wn2=1 + 0.2 * rng.standard_normal(sh.H),
-                       eps=1e-5, rope_base=50.0)
+                       eps=1e-5, rope_base=50.0, bqkv=0.5 * rng.standard_normal(sh.qkv_cols))
     return p, norms
 
 
-@pytest.mark.parametrize("which", ["X", "Wqkv", "Wo", "Wgu", "Wd", "wn1", "wn2"])
+@pytest.mark.parametrize("which", ["X", "Wqkv", "Wo", "Wgu", "Wd", "wn1", "wn2", "bqkv"])
 def test_full_layer_finite_differences(which):
     p, norms = _full_params(8)
 
     def loss(val):
         q = dict(p)
         n = norms
-        if which in ("wn1", "wn2"):
+        if which in ("wn1", "wn2", "bqkv"):
             n = LayerNorms(**{**norms.__dict__, which: val})
         else:
             q[which] = val
@@ -170,8 +175,8 @@ def test_full_layer_finite_differences(which):
 
     g = layer_bwd(SHAPE, p["X"], p["Wqkv"], p["Wo"], p["Wgu"], p["Wd"], p["dY"], norm=norms)
     key = {"X": "dX", "Wqkv": "dWqkv", "Wo": "dWo", "Wgu": "dWgu", "Wd": "dWd",
-           "wn1": "dWn1", "wn2": "dWn2"}[which]
-    start = getattr(norms, which) if which in ("wn1", "wn2") else p[which]
+           "wn1": "dWn1", "wn2": "dWn2", "bqkv": "dbqkv"}[which]
+    start = getattr(norms, which) if which in ("wn1", "wn2", "bqkv") else p[which]
     fd = _fd_grad(loss, np.array(start, dtype=np.float64))
     assert rel_f(g[key], fd) <= 1e-6
 
@@ -191,3 +196,49 @@ def test_planted_rope_sign_mistake_fails_fd():
         return float(np.sum(layer_fwd(SHAPE, x, p["Wqkv"], p["Wo"], p["Wgu"], p["Wd"], norm=norms)["Y"] * p["dY"]))
     fd = _fd_grad(loss, p["X"].copy())
     assert rel_f(g["dX"], fd) > 1e-3
+
+
+def test_column_sum_brute_force():
+    x = np.arange(12, dtype=np.float64).reshape(4, 3) - 5.5
+    want = [sum(x[r][c] for r in range(4)) for c in range(3)]
+    assert np.array_equal(column_sum(x), np.array(want))
+    assert column_sum(np.zeros((0, 3))).tolist() == [0.0, 0.0, 0.0]
+
+
+def test_qkv_bias_only_v_gives_v_bias():
+    """Wqkv = 0 and a bias on the V columns only: every row of every head's
+    attention output is its kv head's V bias (GQA: query head h reads kv head
+    h // (Hq / Hkv)), whatever the scores."""
+    p, norms = _full_params(10)
+    sh = SHAPE
+    b = np.zeros(sh.qkv_cols)
+    bv = np.arange(sh.Hkv * sh.D, dtype=np.float64) * 0.25 - 1.0
+    b[(sh.Hq + sh.Hkv) * sh.D:] = bv
+    n = LayerNorms(**{**norms.__dict__, "bqkv": b})
+    O = layer_fwd(sh, p["X"], np.zeros_like(p["Wqkv"]), p["Wo"], p["Wgu"], p["Wd"], norm=n)["O"]
+    g = sh.Hq // sh.Hkv
+    want = np.concatenate([bv[(h // g) * sh.D:(h // g + 1) * sh.D] for h in range(sh.Hq)])
+    assert np.allclose(O, np.broadcast_to(want, O.shape), rtol=0, atol=1e-12)
+
+
+def test_qkv_bias_is_added_before_the_rotation():
+    """Wqkv = 0, Q and K from the bias alone.  Query 1 against key 0 scores
+    (R_1 bq) . bk (the key at position 0 is unrotated); against key 1 the
+    common rotation cancels and the score is bq . bk.  A bias added after the
+    rotation would give bq . bk for both (LSE = log 2 + that score)."""
+    p, norms = _full_params(11)
+    sh = SHAPE
+    rng = np.random.default_rng(12)
+    bq = rng.standard_normal(sh.D)
+    bk = rng.standard_normal(sh.D)
+    b = np.zeros(sh.qkv_cols)
+    b[:sh.Hq * sh.D] = np.tile(bq, sh.Hq)
+    b[sh.Hq * sh.D:(sh.Hq + sh.Hkv) * sh.D] = np.tile(bk, sh.Hkv)
+    n = LayerNorms(**{**norms.__dict__, "bqkv": b})
+    lse = layer_fwd(sh, p["X"], np.zeros_like(p["Wqkv"]), p["Wo"], p["Wgu"], p["Wd"], norm=n)["LSE"]
+    scale = 1.0 / np.sqrt(sh.D)
+    q_at_1 = rope_fwd(np.stack([bq, bq])[None, :, None, :], norms.rope_base)[0, 1, 0]
+    s10, s11 = scale * float(q_at_1 @ bk), scale * float(bq @ bk)
+    assert abs(lse[0, 0, 1] - np.logaddexp(s10, s11)) <= 1e-12
+    assert abs(lse[0, 0, 0] - s11) <= 1e-12
+    assert abs(lse[0, 0, 1] - (np.log(2.0) + s11)) > 1e-3
