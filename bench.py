@@ -337,6 +337,8 @@ def main():
             "rmsnorm_bwd_gbs": round(2 * (8 * w.T * w.H) / ((avg["rmsnorm1_bwd"] + avg["rmsnorm2_bwd"]) * 1e-3) / 1e9, 1),
             "rope_gbs": round(2 * (4 * w.T * (w.Hq + w.Hkv) * w.D) / ((avg["rope_fwd"] + avg["rope_bwd"]) * 1e-3) / 1e9, 1)}
            if full else {}),
+        **({"qkv_bias_grad_gbs": round(2 * w.T * w.qkv_cols / (avg["qkv_bias_grad"] * 1e-3) / 1e9, 1)}
+           if "qkv_bias_grad" in avg else {}),
         "wall_s": round(wall, 3),
     }
     print("[bench] " + json.dumps(detail), file=sys.stderr, flush=True)
@@ -360,7 +362,9 @@ def main():
         "dtype": "f16",
         "data": "synthetic (seeded N(0,1) activations/grads, N(0,0.02^2) weights, fp16)",
         "config": {"workload": f"{w.name} decoder layer fwd+bwd"
-                               + (" (with RMSNorm and rotary embedding)" if full else ""),
+                               + ((" (with RMSNorm, rotary embedding and QKV bias)"
+                                   if L.bqkv is not None else
+                                   " (with RMSNorm and rotary embedding)") if full else ""),
                    "B": w.B, "S": w.S, "H": w.H,
                    "Hq": w.Hq, "Hkv": w.Hkv, "D": w.D, "F": w.F, "causal": True,
                    "flops_per_step": fl["total"], "parallelism": "single GPU"},

@@ -107,6 +107,38 @@ lt_status lt_gemm_f16_res(int transA, int transB, int64_t M, int64_t N,
                           lt_half* C, int64_t ldc, lt_stream stream);
 
 /*
+ * GEMM with a bias broadcast over the rows (the biased linear layers of the
+ * evaluated Qwen2.5 models, Sec. 6.1: its QKV projection):
+ *
+ *     C[M,N] = alpha * op(A) op(B) + beta * R[M,N] + bias[N]
+ *
+ *   Same conventions and errors as lt_gemm_f16_res; bias is [N] FP16, read
+ *   by every row, 16-byte aligned (else LT_ERR_UNSUPPORTED), never NULL
+ *   (LT_ERR_INVALID_ARG).  The bias is added in FP32 before the single
+ *   rounding of C.
+ */
+lt_status lt_gemm_f16_bias(int transA, int transB, int64_t M, int64_t N,
+                           int64_t K, float alpha, const lt_half* A,
+                           int64_t lda, const lt_half* B, int64_t ldb,
+                           float beta, const lt_half* R, int64_t ldr,
+                           const lt_half* bias, lt_half* C, int64_t ldc,
+                           lt_stream stream);
+
+/*
+ * Bias gradient of a linear layer: db[n] = sum over t < T of dY[t][n]
+ * (dY row-major [T, N] with row stride lddy).  FP32 sums in a fixed order
+ * (deterministic), one rounding to FP16.  The caller-owned workspace, of at
+ * least lt_bias_grad_workspace_size(T, N) bytes (16-byte aligned), holds FP32
+ * partial sums.  Errors: T == 0 or NULL pointers -> LT_ERR_INVALID_ARG
+ * (N == 0 is a no-op); N or lddy not a multiple of 8, dY not 16-byte
+ * aligned -> LT_ERR_UNSUPPORTED; workspace too small -> LT_ERR_WORKSPACE.
+ */
+size_t lt_bias_grad_workspace_size(int64_t T, int64_t N);
+lt_status lt_bias_grad_f16(const lt_half* dY, int64_t lddy, int64_t T, int64_t N,
+                           lt_half* db, void* workspace, size_t ws_bytes,
+                           lt_stream stream);
+
+/*
  * Attention forward (the forward whose probabilities Algorithm 1 consumes;
  * Sec. 4.1).  Per batch b and query head h, with key/value head
  * kv = h / (Hq / Hkv) (contiguous GQA grouping):

@@ -190,7 +190,8 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
                 const lt_half* __restrict__ A, int64_t lda,
                 const lt_half* __restrict__ B, int64_t ldb, float beta,
                 const lt_half* R, int64_t ldr, lt_half* C, int64_t ldc, int tiles_m,
-                int tiles_n, int group_m, lt_half* X1, int64_t ldx1, int64_t F) {
+                int tiles_n, int group_m, lt_half* X1, int64_t ldx1, int64_t F,
+                const lt_half* bias) {
   constexpr int NT = WGM * WGN * kWave;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;   // wave tile
   constexpr int TM = WTM / 16, TN = WTN / 16;     // 16x16 MFMA blocks per wave
@@ -385,6 +386,16 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
     const int64_t nb = n0 + wn * WTN + 4 * (lane >> 4);
     half4 in[IG][TN][NL];
     half4 out[IG][TN][NL];
+    // bias (epilogue 0): the same 4 columns for every accumulator row
+    const bool has_bias = EPI == 0 && bias != nullptr;   // uniform over the grid
+    half4 bv[TN];
+    if (has_bias) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int64_t n = nb + j * 16;
+        bv[j] = *reinterpret_cast<const half4*>(bias + (n < N ? n : N - 4));
+      }
+    }
 
     // loads are unconditional, from addresses clamped into the matrix
     // (values of out-of-range blocks are never stored): no branch between
@@ -430,6 +441,10 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
 #pragma unroll
               for (int e = 0; e < 4; ++e) v[e] += beta * (float)in[ii][j][0][e];
             }
+            if (has_bias) {
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] += (float)bv[j][e];
+            }
 #pragma unroll
             for (int e = 0; e < 4; ++e) out[ii][j][0][e] = (_Float16)v[e];
           }
@@ -466,7 +481,7 @@ hipError_t launch(const GemmArgs& g, hipStream_t s) {
   hipLaunchKernelGGL((gemm_f16_kernel<BM, BN, WGM, WGN, BK, NS, TA, TB, EPI>),
                      dim3(tiles_m * tiles_n), dim3(WGM * WGN * kWave), 0, s, g.M, g.N, g.K, g.alpha,
                      g.A, g.lda, g.B, g.ldb, g.beta, g.R, g.ldr, g.C, g.ldc, tiles_m, tiles_n, 8,
-                     g.X1, g.ldx1, g.F);
+                     g.X1, g.ldx1, g.F, g.bias);
   return hipGetLastError();
 }
 

@@ -30,6 +30,8 @@ struct GemmArgs {
   lt_half* X1 = nullptr;
   int64_t ldx1 = 0;
   int64_t F = 0;
+  // optional bias [N] added to every row (epilogue 0 only)
+  const lt_half* bias = nullptr;
 };
 
 struct AttnShape {
@@ -117,7 +119,18 @@ inline size_t rmsnorm_bwd_ws_bytes(int64_t T, int64_t H) {
   return align256((size_t)rmsnorm_bwd_blocks(T) * 4 * H * sizeof(float));
 }
 
+// bias gradient (column sum): FP32 partial rows of the workspace
+inline int bias_grad_blocks(int64_t T) {
+  const int64_t b = (T + 63) / 64;
+  return (int)(b < 128 ? (b < 1 ? 1 : b) : 128);
+}
+inline size_t bias_grad_ws_bytes(int64_t T, int64_t N) {
+  return align256((size_t)bias_grad_blocks(T) * (size_t)N * sizeof(float));
+}
+
 hipError_t gemm_f16_launch(const GemmArgs& a, hipStream_t s);
+hipError_t bias_grad_launch(const lt_half* dY, int64_t lddy, int64_t T, int64_t N, lt_half* db,
+                            float* part, hipStream_t s);
 hipError_t attn_fwd_launch(const AttnFwdArgs& a, hipStream_t s);
 hipError_t attn_bwd_launch(const AttnBwdArgs& a, hipStream_t s);
 hipError_t rmsnorm_fwd_launch(const lt_half* X, int64_t ldx, const lt_half* W, lt_half* Y,

@@ -62,27 +62,10 @@ lt_status check_attn_common(const void* Q, const void* K, const void* V, int64_t
 
 }  // namespace
 
-extern "C" {
-
-const char* lt_status_string(lt_status s) {
-  switch (s) {
-    case LT_OK: return "LT_OK";
-    case LT_ERR_INVALID_ARG: return "LT_ERR_INVALID_ARG";
-    case LT_ERR_UNSUPPORTED: return "LT_ERR_UNSUPPORTED";
-    case LT_ERR_WORKSPACE: return "LT_ERR_WORKSPACE";
-    case LT_ERR_HIP: return "LT_ERR_HIP";
-  }
-  return "LT_ERR_UNKNOWN";
-}
-
-const char* lt_last_error(void) { return g_last_error.c_str(); }
-
-int lt_version(void) { return 100; }
-
-lt_status lt_gemm_f16_res(int transA, int transB, int64_t M, int64_t N, int64_t K, float alpha,
-                          const lt_half* A, int64_t lda, const lt_half* B, int64_t ldb, float beta,
-                          const lt_half* R, int64_t ldr, lt_half* C, int64_t ldc,
-                          lt_stream stream) {
+static lt_status gemm_common(int transA, int transB, int64_t M, int64_t N, int64_t K, float alpha,
+                             const lt_half* A, int64_t lda, const lt_half* B, int64_t ldb,
+                             float beta, const lt_half* R, int64_t ldr, const lt_half* bias,
+                             lt_half* C, int64_t ldc, lt_stream stream) {
   if ((transA != 0 && transA != 1) || (transB != 0 && transB != 1))
     return fail(LT_ERR_INVALID_ARG, "transA/transB must be 0 or 1");
   if (M < 0 || N < 0 || K < 0) return fail(LT_ERR_INVALID_ARG, "negative GEMM size");
@@ -106,9 +89,70 @@ lt_status lt_gemm_f16_res(int transA, int transB, int64_t M, int64_t N, int64_t 
     return fail(LT_ERR_UNSUPPORTED, "M, N or K too large for the tile grid");
   if (lda >= ((int64_t)1 << 22) || ldb >= ((int64_t)1 << 22))
     return fail(LT_ERR_UNSUPPORTED, "lda/ldb must be < 2^22 elements (32-bit buffer offsets)");
+  if (bias && !aligned16(bias)) return fail(LT_ERR_UNSUPPORTED, "bias must be 16-byte aligned");
   lt::GemmArgs g{transA, transB, M, N, K, alpha, beta, A, lda, B, ldb,
                  beta != 0.f ? R : C, beta != 0.f ? ldr : ldc, C, ldc};
+  g.bias = bias;
   return from_hip(lt::gemm_f16_launch(g, reinterpret_cast<hipStream_t>(stream)), "gemm launch");
+}
+
+extern "C" {
+
+const char* lt_status_string(lt_status s) {
+  switch (s) {
+    case LT_OK: return "LT_OK";
+    case LT_ERR_INVALID_ARG: return "LT_ERR_INVALID_ARG";
+    case LT_ERR_UNSUPPORTED: return "LT_ERR_UNSUPPORTED";
+    case LT_ERR_WORKSPACE: return "LT_ERR_WORKSPACE";
+    case LT_ERR_HIP: return "LT_ERR_HIP";
+  }
+  return "LT_ERR_UNKNOWN";
+}
+
+const char* lt_last_error(void) { return g_last_error.c_str(); }
+
+int lt_version(void) { return 100; }
+
+lt_status lt_gemm_f16_res(int transA, int transB, int64_t M, int64_t N, int64_t K, float alpha,
+                          const lt_half* A, int64_t lda, const lt_half* B, int64_t ldb, float beta,
+                          const lt_half* R, int64_t ldr, lt_half* C, int64_t ldc,
+                          lt_stream stream) {
+  return gemm_common(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, R, ldr, nullptr, C,
+                     ldc, stream);
+}
+
+lt_status lt_gemm_f16_bias(int transA, int transB, int64_t M, int64_t N, int64_t K, float alpha,
+                           const lt_half* A, int64_t lda, const lt_half* B, int64_t ldb,
+                           float beta, const lt_half* R, int64_t ldr, const lt_half* bias,
+                           lt_half* C, int64_t ldc, lt_stream stream) {
+  if (!bias && M > 0 && N > 0) return fail(LT_ERR_INVALID_ARG, "NULL bias");
+  return gemm_common(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, R, ldr, bias, C, ldc,
+                     stream);
+}
+
+size_t lt_bias_grad_workspace_size(int64_t T, int64_t N) {
+  if (T < 1 || N < 1) return 0;
+  return lt::bias_grad_ws_bytes(T, N);
+}
+
+lt_status lt_bias_grad_f16(const lt_half* dY, int64_t lddy, int64_t T, int64_t N, lt_half* db,
+                           void* workspace, size_t ws_bytes, lt_stream stream) {
+  if (T < 0 || N < 0) return fail(LT_ERR_INVALID_ARG, "negative size");
+  if (N == 0) return ok();
+  if (!db) return fail(LT_ERR_INVALID_ARG, "NULL db");
+  if (T == 0) return fail(LT_ERR_INVALID_ARG, "T == 0: the bias gradient needs at least one row");
+  if (!dY) return fail(LT_ERR_INVALID_ARG, "NULL dY");
+  if (lddy < N) return fail(LT_ERR_INVALID_ARG, "lddy < N");
+  if ((N & 7) || (lddy & 7)) return fail(LT_ERR_UNSUPPORTED, "N and lddy must be multiples of 8");
+  if (!aligned16(dY)) return fail(LT_ERR_UNSUPPORTED, "dY must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(db) & 1u) return fail(LT_ERR_UNSUPPORTED, "db must be 2-byte aligned");
+  if (!workspace || ws_bytes < lt::bias_grad_ws_bytes(T, N))
+    return fail(LT_ERR_WORKSPACE, "workspace needs %zu bytes", lt::bias_grad_ws_bytes(T, N));
+  if (reinterpret_cast<uintptr_t>(workspace) & 15u)
+    return fail(LT_ERR_UNSUPPORTED, "workspace must be 16-byte aligned");
+  return from_hip(lt::bias_grad_launch(dY, lddy, T, N, db, static_cast<float*>(workspace),
+                                       reinterpret_cast<hipStream_t>(stream)),
+                  "bias_grad launch");
 }
 
 lt_status lt_gemm_f16(int transA, int transB, int64_t M, int64_t N, int64_t K, float alpha,

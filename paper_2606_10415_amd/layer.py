@@ -17,6 +17,9 @@ rotated in place in QKV, and the backward runs the inverse rotation on dQ, dK
 and RMSNorm backward (with the residual gradient added in the same pass):
     dH1 = dY + rmsnorm_bwd(dGU Wgu) ;  dX = dH1 + rmsnorm_bwd(dQKV Wqkv)
 
+A norm with a QKV bias (Qwen2.5) adds it in the QKV GEMM's epilogue and
+takes its gradient as the column sum of dQKV after the inverse rotation.
+
 With ``fuse_swiglu`` the SwiGLU gate runs in the epilogues of the gate/up
 GEMM (A from the FP32 accumulators, GU still stored for the backward) and of
 the down-projection dgrad (dGU written directly, dA never stored).
@@ -34,7 +37,8 @@ class DecoderLayer:
 
     ``shape`` needs attributes B, S, H, Hq, Hkv, D, F.  ``params`` maps
     X, dY, Wqkv, Wo, Wgu, Wd to float16 tensors (host or device).  ``norm``
-    (optional) has attributes wn1, wn2 (RMSNorm weights [H]), eps, rope_base.
+    (optional) has attributes wn1, wn2 (RMSNorm weights [H]), eps, rope_base and
+    optionally bqkv (QKV projection bias, or None).
     ``fuse_swiglu`` selects the GEMMs with the SwiGLU epilogues.
     """
 
@@ -98,6 +102,12 @@ class DecoderLayer:
             lt.lt_rope_table(self.CS, sh.S, sh.D, float(norm.rope_base))
             self.rms_ws_bytes = lt.lt_rmsnorm_bwd_workspace_size(T, sh.H)
             self.rms_ws = torch.empty(self.rms_ws_bytes, dtype=torch.uint8, device=self.dev)
+        self.bqkv = None
+        if norm is not None and getattr(norm, "bqkv", None) is not None:
+            self.bqkv = dev(norm.bqkv)
+            self.dbqkv = e(self.qkv)
+            self.bias_ws_bytes = lt.lt_bias_grad_workspace_size(T, self.qkv)
+            self.bias_ws = torch.empty(self.bias_ws_bytes, dtype=torch.uint8, device=self.dev)
 
     # ------------------------------------------------------------ steps
     def _attn_ptrs(self, base):
@@ -114,8 +124,12 @@ class DecoderLayer:
                               stream)
             mark("rmsnorm1_fwd")
             xin = self.Xn
-        lt.lt_gemm_f16(0, 1, T, self.qkv, sh.H, 1.0, xin, sh.H, self.Wqkv, sh.H, 0.0,
-                       self.QKV, self.qkv, stream)
+        if self.bqkv is not None:
+            lt.lt_gemm_f16_bias(0, 1, T, self.qkv, sh.H, 1.0, xin, sh.H, self.Wqkv, sh.H, 0.0, None,
+                                self.qkv, self.bqkv, self.QKV, self.qkv, stream)
+        else:
+            lt.lt_gemm_f16(0, 1, T, self.qkv, sh.H, 1.0, xin, sh.H, self.Wqkv, sh.H, 0.0,
+                           self.QKV, self.qkv, stream)
         mark("qkv_fwd")
         if self.norm is not None:
             lt.lt_rope_f16(self.QKV, self.qkv, sh.B, sh.S, sh.Hq + sh.Hkv, sh.D, self.CS, 0, stream)
@@ -198,6 +212,10 @@ class DecoderLayer:
         if self.norm is not None:
             lt.lt_rope_f16(self.dQKV, self.qkv, sh.B, sh.S, sh.Hq + sh.Hkv, sh.D, self.CS, 1, stream)
             mark("rope_bwd")
+        if self.bqkv is not None:
+            lt.lt_bias_grad_f16(self.dQKV, self.qkv, T, self.qkv, self.dbqkv, self.bias_ws,
+                                self.bias_ws_bytes, stream)
+            mark("qkv_bias_grad")
         # QKV projection
         xin = self.Xn if self.norm is not None else self.X
         lt.lt_gemm_f16(1, 0, self.qkv, sh.H, T, 1.0, self.dQKV, self.qkv, xin, sh.H, 0.0,

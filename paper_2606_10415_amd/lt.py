@@ -86,6 +86,13 @@ _lib.lt_swiglu_fwd.restype = _int
 _lib.lt_swiglu_fwd.argtypes = [_vp, _vp, _i64, _i64, _vp]
 _lib.lt_swiglu_bwd.restype = _int
 _lib.lt_swiglu_bwd.argtypes = [_vp, _vp, _vp, _i64, _i64, _vp]
+_lib.lt_gemm_f16_bias.restype = _int
+_lib.lt_gemm_f16_bias.argtypes = [_int, _int, _i64, _i64, _i64, ctypes.c_float, _vp, _i64, _vp, _i64,
+                                  ctypes.c_float, _vp, _i64, _vp, _vp, _i64, _vp]
+_lib.lt_bias_grad_workspace_size.restype = ctypes.c_size_t
+_lib.lt_bias_grad_workspace_size.argtypes = [_i64, _i64]
+_lib.lt_bias_grad_f16.restype = _int
+_lib.lt_bias_grad_f16.argtypes = [_vp, _i64, _i64, _i64, _vp, _vp, ctypes.c_size_t, _vp]
 _lib.lt_gemm_gu_swiglu_f16.restype = _int
 _lib.lt_gemm_gu_swiglu_f16.argtypes = [_vp, _i64, _vp, _i64, _vp, _i64, _vp, _i64, _i64, _i64, _i64, _vp]
 _lib.lt_gemm_swiglu_bwd_f16.restype = _int
@@ -183,6 +190,23 @@ def lt_swiglu_fwd(GU, A, T, F, stream=None):
 def lt_swiglu_bwd(dA, GU, dGU, T, F, stream=None):
     _check(_lib.lt_swiglu_bwd(_ptr(dA), _ptr(GU), _ptr(dGU), int(T), int(F), _stream(stream)),
            "lt_swiglu_bwd")
+
+
+def lt_gemm_f16_bias(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, R, ldr, bias, C, ldc,
+                     stream=None):
+    _check(_lib.lt_gemm_f16_bias(int(transA), int(transB), int(M), int(N), int(K), float(alpha),
+                                 _ptr(A), int(lda), _ptr(B), int(ldb), float(beta), _ptr(R),
+                                 int(ldr), _ptr(bias), _ptr(C), int(ldc), _stream(stream)),
+           "lt_gemm_f16_bias")
+
+
+def lt_bias_grad_workspace_size(T, N):
+    return int(_lib.lt_bias_grad_workspace_size(int(T), int(N)))
+
+
+def lt_bias_grad_f16(dY, lddy, T, N, db, workspace, ws_bytes, stream=None):
+    _check(_lib.lt_bias_grad_f16(_ptr(dY), int(lddy), int(T), int(N), _ptr(db), _ptr(workspace),
+                                 int(ws_bytes), _stream(stream)), "lt_bias_grad_f16")
 
 
 def lt_gemm_gu_swiglu_f16(X, ldx, Wgu, ldw, GU, ldgu, A, lda, T, H, F, stream=None):

@@ -15,7 +15,8 @@ def test_every_declared_symbol_is_exported():
             "lt_attn_bwd_workspace_size", "lt_swiglu_fwd", "lt_swiglu_bwd",
             "lt_status_string", "lt_last_error", "lt_version", "lt_rmsnorm_fwd",
             "lt_rmsnorm_bwd", "lt_rmsnorm_bwd_workspace_size", "lt_rope_table",
-            "lt_rope_f16", "lt_gemm_gu_swiglu_f16", "lt_gemm_swiglu_bwd_f16"} <= set(names)
+            "lt_rope_f16", "lt_gemm_gu_swiglu_f16", "lt_gemm_swiglu_bwd_f16", "lt_gemm_f16_bias",
+            "lt_bias_grad_workspace_size", "lt_bias_grad_f16"} <= set(names)
     for n in names:
         assert hasattr(lt._lib, n), f"{n} declared in lt.h but not exported"
 
@@ -250,3 +251,40 @@ def test_gemm_swiglu_bwd_rejects_on_host(kw, status):
 def test_fused_swiglu_empty_is_noop():
     assert lt._lib.lt_gemm_gu_swiglu_f16(None, 8, None, 8, None, 0, None, 0, 0, 8, 8, None) == lt.LT_OK
     assert lt._lib.lt_gemm_swiglu_bwd_f16(None, 8, None, 8, None, 0, None, 0, 8, 8, 0, None) == lt.LT_OK
+
+
+def test_gemm_bias_rejects_on_host():
+    g = lambda **kw: lt._lib.lt_gemm_f16_bias(
+        0, 1, kw.get("M", 64), 64, 64, 1.0, FAKE, 64, FAKE, 64, 0.0, None, 64, kw.get("bias", FAKE),
+        FAKE, 64, None)
+    assert g(bias=None) == lt.LT_ERR_INVALID_ARG
+    assert g(bias=FAKE + 2) == lt.LT_ERR_UNSUPPORTED
+    assert g(M=60) == lt.LT_ERR_UNSUPPORTED
+    assert g(M=0, bias=None) == lt.LT_OK          # empty: no-op
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(T=0), lt.LT_ERR_INVALID_ARG),
+    (dict(T=-1), lt.LT_ERR_INVALID_ARG),
+    (dict(dY=None), lt.LT_ERR_INVALID_ARG),
+    (dict(db=None), lt.LT_ERR_INVALID_ARG),
+    (dict(lddy=32), lt.LT_ERR_INVALID_ARG),
+    (dict(N=60, lddy=64), lt.LT_ERR_UNSUPPORTED),
+    (dict(lddy=68), lt.LT_ERR_UNSUPPORTED),
+    (dict(dY=FAKE + 2), lt.LT_ERR_UNSUPPORTED),
+    (dict(ws=None), lt.LT_ERR_WORKSPACE),
+    (dict(wsb=16), lt.LT_ERR_WORKSPACE),
+    (dict(ws=FAKE + 8), lt.LT_ERR_UNSUPPORTED),
+])
+def test_bias_grad_rejects_on_host(kw, status):
+    a = dict(dY=FAKE, lddy=64, T=100, N=64, db=FAKE, ws=FAKE, wsb=1 << 20)
+    a.update(kw)
+    st = lt._lib.lt_bias_grad_f16(a["dY"], a["lddy"], a["T"], a["N"], a["db"], a["ws"], a["wsb"], None)
+    assert st == status
+
+
+def test_bias_grad_workspace_and_empty():
+    assert lt.lt_bias_grad_workspace_size(0, 64) == 0
+    assert lt.lt_bias_grad_workspace_size(4096, 7168) == 64 * 7168 * 4
+    assert lt.lt_bias_grad_workspace_size(1, 8) % 256 == 0
+    assert lt._lib.lt_bias_grad_f16(None, 0, 5, 0, None, None, 0, None) == lt.LT_OK

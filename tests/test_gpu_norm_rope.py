@@ -1,13 +1,14 @@
 """GPU parity of RMSNorm, the rotary embedding and the full (normed, rotated)
 decoder layer against the float64 oracle.
 
-Bars: per op (same fp16 inputs) RMSNorm y, dx, dw and the rotated Q/K
-relative Frobenius error <= 5e-3 (one fp16 rounding of an FP32 result);
+Bars: per op (same fp16 inputs) RMSNorm y, dx, dw, the rotated Q/K, the
+biased GEMM and the bias gradient relative Frobenius error <= 5e-3 (one fp16
+rounding of an FP32 result);
 RMSNorm rstd <= 1e-5 relative (FP32 sums); rotation table <= 1e-6 absolute
 (FP32 rounding of FP64 cos/sin); V columns of the fused buffer untouched
 (bitwise).  Chained full layer (fp16 intermediates on the GPU, float64 in the
-oracle): Y, dX, the four projection weight gradients and both RMSNorm weight
-gradients <= 5e-3, dQKV <= 1e-2.
+oracle): Y, dX, the four projection weight gradients, both RMSNorm weight
+gradients and the QKV bias gradient (Qwen family) <= 5e-3, dQKV <= 1e-2.
 """
 
 import numpy as np
@@ -106,7 +107,8 @@ def test_full_layer_chained_parity(env, w, family, fuse):
     torch.cuda.synchronize()
     sh = oracle.LayerShape(w.B, w.S, w.H, w.Hq, w.Hkv, w.D, w.F)
     norms = oracle.LayerNorms(wn1=n.wn1.astype(np.float64), wn2=n.wn2.astype(np.float64),
-                              eps=n.eps, rope_base=n.rope_base)
+                              eps=n.eps, rope_base=n.rope_base,
+                              bqkv=None if n.bqkv is None else n.bqkv.astype(np.float64))
     acts = oracle.layer_fwd(sh, p["X"], p["Wqkv"], p["Wo"], p["Wgu"], p["Wd"], norm=norms)
     grads = oracle.layer_bwd(sh, p["X"], p["Wqkv"], p["Wo"], p["Wgu"], p["Wd"], p["dY"], acts,
                              norm=norms)
@@ -115,6 +117,54 @@ def test_full_layer_chained_parity(env, w, family, fuse):
     for name in ("dWqkv", "dWo", "dWgu", "dWd", "dWn1", "dWn2"):
         err[name] = rel_f(c(getattr(L, name)), grads[name])
     err["dQKV"] = rel_f(c(L.dQKV), grads["dQKV"])
+    if n.bqkv is not None:
+        err["dbqkv"] = rel_f(c(L.dbqkv), grads["dbqkv"])
     print("  errors: " + ", ".join(f"{k} {v:.3e}" for k, v in err.items()), flush=True)
     for k, v in err.items():
         assert v <= (1e-2 if k == "dQKV" else 5e-3), k
+
+
+@pytest.mark.parametrize("M,N,K,beta", [(296, 520, 136, 0.0), (72, 1032, 512, 1.0), (8, 8, 8, 0.0),
+                                        (4096, 7168, 5120, 0.0)])
+def test_gemm_bias_parity(env, M, N, K, beta):
+    """C = A B^T + beta R + bias (the biased QKV projection); full size on sampled rows."""
+    print(f"gemm bias M={M} N={N} K={K} beta={beta}", flush=True)
+    torch, lt = env
+    a = normal_f16(71, (M, K))
+    b = normal_f16(72, (N, K), 0.02)
+    bias = normal_f16(73, (N,), 0.5)
+    r = normal_f16(74, (M, N))
+    cu = lambda x: torch.from_numpy(x).cuda()
+    C = torch.full((M, N), float("nan"), dtype=torch.float16, device="cuda")
+    lt.lt_gemm_f16_bias(0, 1, M, N, K, 1.0, cu(a), K, cu(b), K, beta, cu(r) if beta else None, N,
+                        cu(bias), C, N)
+    torch.cuda.synchronize()
+    rows = np.arange(M) if M <= 1024 else np.unique(np.concatenate(
+        [np.random.default_rng(5).choice(M, 40, replace=False), [0, M - 1]]))
+    want = oracle.gemm(0, 1, 1.0, a[rows], b, beta, r[rows] if beta else None) + bias.astype(np.float64)
+    err = rel_f(C.cpu().numpy()[rows], want)
+    print(f"  err {err:.3e}", flush=True)
+    assert err <= 5e-3
+
+
+@pytest.mark.parametrize("T,N,ld", [(4096, 7168, 7168), (1, 8, 8), (1000, 520, 528), (65, 6144, 6144),
+                                    (8192, 10240, 10240)])
+def test_bias_grad_parity(env, T, N, ld):
+    print(f"bias grad T={T} N={N} ld={ld}", flush=True)
+    torch, lt = env
+    dy = normal_f16(75, (T, ld))
+    wsb = lt.lt_bias_grad_workspace_size(T, N)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    db = torch.full((N,), float("nan"), dtype=torch.float16, device="cuda")
+    dY = torch.from_numpy(dy).cuda()
+    lt.lt_bias_grad_f16(dY, ld, T, N, db, ws, wsb)
+    db2 = torch.empty_like(db)
+    lt.lt_bias_grad_f16(dY, ld, T, N, db2, ws, wsb)
+    torch.cuda.synchronize()
+    want = oracle.column_sum(dy[:, :N])
+    got = db.cpu().numpy()
+    err = rel_f(got, want)
+    print(f"  err {err:.3e}", flush=True)
+    assert err <= 5e-3
+    assert np.max(np.abs(got.astype(np.float64) - want)) <= 2e-3 * np.sqrt(T) + 1e-3 * np.max(np.abs(want))
+    assert torch.equal(db.view(torch.int16), db2.view(torch.int16))     # deterministic
