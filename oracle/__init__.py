@@ -19,6 +19,9 @@ preserves the model computation exactly; Sec. 4.1 and Sec. 5.3):
                     models (Sec. 6.1) and their gradients
 * ``layer``      -- one decoder layer forward + backward composed of the above
                     (optionally with the models' RMSNorm and rotary embedding)
+* ``pipeline``   -- the non-interleaved 1F1B schedule as a discrete-event
+                    simulation (makespan, resident micro-batches per stage;
+                    Sec. 4.3-4.4), the reference for the planner
 
 No blocking, fusion, online softmax or reordering: a reader can check each
 function against the definitions by eye.  Library primitives used as single
@@ -34,6 +37,7 @@ from .attention import attn_fwd, attn_bwd, attn_head_fwd, attn_head_bwd
 from .swiglu import silu, swiglu_fwd, swiglu_bwd
 from .norm_rope import rmsnorm_fwd, rmsnorm_bwd, rope_angles, rope_fwd, rope_bwd
 from .layer import LayerShape, LayerNorms, layer_fwd, layer_bwd, layer_flops
+from .pipeline import stage_order, simulate_1f1b
 
 __all__ = [
     "gemm", "gemm_entries", "column_sum",
@@ -41,4 +45,5 @@ __all__ = [
     "silu", "swiglu_fwd", "swiglu_bwd",
     "rmsnorm_fwd", "rmsnorm_bwd", "rope_angles", "rope_fwd", "rope_bwd",
     "LayerShape", "LayerNorms", "layer_fwd", "layer_bwd", "layer_flops",
+    "stage_order", "simulate_1f1b",
 ]
