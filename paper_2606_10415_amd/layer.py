@@ -42,9 +42,11 @@ class DecoderLayer:
     ``fuse_swiglu`` selects the GEMMs with the SwiGLU epilogues.
     """
 
-    def __init__(self, shape, params, device="cuda", norm=None, fuse_swiglu=True):
+    def __init__(self, shape, params, device="cuda", norm=None, fuse_swiglu=True,
+                 share_bwd=None, share_acts=None):
         self.sh = sh = shape
         self.fuse_swiglu = bool(fuse_swiglu)
+        self.accumulate = False
         self.dev = torch.device(device)
         T = sh.B * sh.S
         self.T = T
@@ -56,33 +58,44 @@ class DecoderLayer:
             t = x if isinstance(x, torch.Tensor) else torch.from_numpy(x)
             return t.to(self.dev, torch.float16).contiguous()
 
-        self.X = dev(params["X"])
-        self.dY = dev(params["dY"])
+        self.X = dev(params["X"]) if params.get("X") is not None else None
+        self.dY = dev(params["dY"]) if params.get("dY") is not None else None
         self.Wqkv = dev(params["Wqkv"])
         self.Wo = dev(params["Wo"])
         self.Wgu = dev(params["Wgu"])
         self.Wd = dev(params["Wd"])
 
         e = lambda *s: torch.empty(*s, dtype=torch.float16, device=self.dev)
-        self.QKV = e(T, self.qkv)
-        self.O = e(T, self.hd)
-        self.LSE = torch.empty(sh.B, sh.Hq, sh.S, dtype=torch.float32, device=self.dev)
-        self.H1 = e(T, sh.H)
-        self.GU = e(T, 2 * sh.F)
-        self.A = e(T, sh.F)
+        # forward activations the backward reads (shareable between layers
+        # whose forward is recomputed right before their backward)
+        if share_acts is not None:
+            for k in ("QKV", "O", "LSE", "H1", "GU", "A"):
+                setattr(self, k, getattr(share_acts, k))
+        else:
+            self.QKV = e(T, self.qkv)
+            self.O = e(T, self.hd)
+            self.LSE = torch.empty(sh.B, sh.Hq, sh.S, dtype=torch.float32, device=self.dev)
+            self.H1 = e(T, sh.H)
+            self.GU = e(T, 2 * sh.F)
+            self.A = e(T, sh.F)
         self.Y = e(T, sh.H)
-        self.dA = e(T, sh.F)
-        self.dGU = e(T, 2 * sh.F)
-        self.dH1 = e(T, sh.H)
-        self.dO = e(T, self.hd)
-        self.dQKV = e(T, self.qkv)
-        self.dX = e(T, sh.H)
+        # backward temporaries (shareable between the layers of a stage)
+        if share_bwd is not None:
+            for k in ("dA", "dGU", "dH1", "dO", "dQKV", "dX", "ws", "ws_bytes"):
+                setattr(self, k, getattr(share_bwd, k))
+        else:
+            self.dA = e(T, sh.F)
+            self.dGU = e(T, 2 * sh.F)
+            self.dH1 = e(T, sh.H)
+            self.dO = e(T, self.hd)
+            self.dQKV = e(T, self.qkv)
+            self.dX = e(T, sh.H)
+            self.ws_bytes = lt.lt_attn_bwd_workspace_size(sh.B, sh.S, sh.Hq, sh.Hkv, sh.D)
+            self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.dev)
         self.dWqkv = e(*self.Wqkv.shape)
         self.dWo = e(*self.Wo.shape)
         self.dWgu = e(*self.Wgu.shape)
         self.dWd = e(*self.Wd.shape)
-        self.ws_bytes = lt.lt_attn_bwd_workspace_size(sh.B, sh.S, sh.Hq, sh.Hkv, sh.D)
-        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.dev)
 
         self.norm = norm
         if norm is not None:
@@ -165,7 +178,10 @@ class DecoderLayer:
         sh, T = self.sh, self.T
         mark = hook or (lambda name: None)
         # down projection
-        lt.lt_gemm_f16(1, 0, sh.H, sh.F, T, 1.0, self.dY, sh.H, self.A, sh.F, 0.0, self.dWd, sh.F,
+        if self.accumulate and (self.norm is not None or self.bqkv is not None):
+            raise ValueError("gradient accumulation covers the four projection weights only")
+        wb = 1.0 if self.accumulate else 0.0     # weight gradients: overwrite or accumulate
+        lt.lt_gemm_f16(1, 0, sh.H, sh.F, T, 1.0, self.dY, sh.H, self.A, sh.F, wb, self.dWd, sh.F,
                        stream)
         mark("down_wgrad")
         if self.fuse_swiglu:
@@ -180,7 +196,7 @@ class DecoderLayer:
             mark("swiglu_bwd")
         # gate/up projection
         hin = self.H1n if self.norm is not None else self.H1
-        lt.lt_gemm_f16(1, 0, 2 * sh.F, sh.H, T, 1.0, self.dGU, 2 * sh.F, hin, sh.H, 0.0,
+        lt.lt_gemm_f16(1, 0, 2 * sh.F, sh.H, T, 1.0, self.dGU, 2 * sh.F, hin, sh.H, wb,
                        self.dWgu, sh.H, stream)
         mark("gu_wgrad")
         if self.norm is not None:
@@ -196,7 +212,7 @@ class DecoderLayer:
                                1.0, self.dY, sh.H, self.dH1, sh.H, stream)
             mark("gu_dgrad")
         # output projection
-        lt.lt_gemm_f16(1, 0, sh.H, self.hd, T, 1.0, self.dH1, sh.H, self.O, self.hd, 0.0, self.dWo,
+        lt.lt_gemm_f16(1, 0, sh.H, self.hd, T, 1.0, self.dH1, sh.H, self.O, self.hd, wb, self.dWo,
                        self.hd, stream)
         mark("o_wgrad")
         lt.lt_gemm_f16(0, 0, T, self.hd, sh.H, 1.0, self.dH1, sh.H, self.Wo, self.hd, 0.0, self.dO,
@@ -218,7 +234,7 @@ class DecoderLayer:
             mark("qkv_bias_grad")
         # QKV projection
         xin = self.Xn if self.norm is not None else self.X
-        lt.lt_gemm_f16(1, 0, self.qkv, sh.H, T, 1.0, self.dQKV, self.qkv, xin, sh.H, 0.0,
+        lt.lt_gemm_f16(1, 0, self.qkv, sh.H, T, 1.0, self.dQKV, self.qkv, xin, sh.H, wb,
                        self.dWqkv, sh.H, stream)
         mark("qkv_wgrad")
         if self.norm is not None:
