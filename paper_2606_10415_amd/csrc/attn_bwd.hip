@@ -187,6 +187,8 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
   if (n_iter > 0) stage(0, 0);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) loaded_here(kf[kk]);
 
   for (int it = 0; it < n_iter; ++it) {
     const int cur = it & 1;
@@ -399,6 +401,13 @@ attn_bwd_dq_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
   if (n_kv > 0) stage_load(0, 0);
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    loaded_here(qf[kk]);
+    loaded_here(of[kk]);
+  }
+  loaded_here(l2);
+  loaded_here(dl);
 
   for (int kt = 0; kt < n_kv; ++kt) {
     const char* ks = smem + (kt & 1) * SM::STAGE;

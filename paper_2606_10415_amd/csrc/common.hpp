@@ -37,6 +37,18 @@ __device__ __forceinline__ f32x4 mfma16(half8 a, half8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
 
+// Registers loaded from global memory before a loop are marked as used at
+// this point: the compiler then waits for their loads here, once, instead of
+// before their first use inside the loop.  That in-loop wait would be a
+// vmcnt(0) executed every iteration, and vmcnt also counts the direct-to-LDS
+// prefetches issued inside the loop (opaque to the compiler), so each
+// iteration would wait for its own prefetch.  Call it after an explicit
+// vmcnt(0), where it costs nothing.
+template <class T>
+__device__ __forceinline__ void loaded_here(const T& v) {
+  asm volatile("" ::"v"(v));
+}
+
 __device__ __forceinline__ half8 as_half8(u32x4 v) {
   return __builtin_bit_cast(half8, v);
 }
