@@ -42,9 +42,9 @@ GEMM_TRAFFIC = {
     "workload": "llama2-7b",
     "layer": "paper",
     "fuse_swiglu": True,
-    "sources_sha256": "cae80934e7977d556bd56b4a976d85943faf5374daa89bb464292c69264615e0",
-    "fetch_bytes_per_launch": 687653039,
-    "write_bytes_per_launch": 94718810,
+    "sources_sha256": "e464e457cd799d4db4173199118ef3dc57dc2125d3a7f640ee09c54fb2316475",
+    "fetch_bytes_per_launch": 687996275,
+    "write_bytes_per_launch": 95126881,
 }
 GEMM_SOURCES = ("paper_2606_10415_amd/csrc/gemm_f16.hip", "paper_2606_10415_amd/csrc/common.hpp")
 
