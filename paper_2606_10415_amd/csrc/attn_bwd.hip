@@ -217,11 +217,27 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
         sacc[r] = 0.f;
         pacc[r] = 0.f;
       }
+      // fragments of step kk+1 are read before the MFMAs of step kk
+      half8 fq = RT::row_frag(qs, hq * 32, 0, lane);
+      half8 fd = RT::row_frag(dos, hq * 32, 0, lane);
+      half8 fv = RT::row_frag(smem + SM::V_OFF, wave * 32, 0, lane);
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
-        sacc = mfma32(RT::row_frag(qs, hq * 32, kk, lane), kf[kk], sacc);
-        pacc = mfma32(RT::row_frag(dos, hq * 32, kk, lane),
-                      RT::row_frag(smem + SM::V_OFF, wave * 32, kk, lane), pacc);
+        half8 nq = fq, nd = fd, nv = fv;
+        if (kk + 1 < KK) {
+          nq = RT::row_frag(qs, hq * 32, kk + 1, lane);
+          nd = RT::row_frag(dos, hq * 32, kk + 1, lane);
+          nv = RT::row_frag(smem + SM::V_OFF, wave * 32, kk + 1, lane);
+        }
+        sacc = mfma32(fq, kf[kk], sacc);
+        pacc = mfma32(fd, fv, pacc);
+        if (kk + 1 < KK) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);   // the three reads
+          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // then the two MFMAs
+        }
+        fq = nq;
+        fd = nd;
+        fv = nv;
       }
 
       float p[16], ds[16];
