@@ -133,11 +133,25 @@ attn_fwd_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
       for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
+      // K fragments of step kk+1 are read before the MFMAs of step kk
+      half8 kfr[KB];
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk)
+      for (int kb = 0; kb < KB; ++kb) kfr[kb] = RT::row_frag(st, kb * 32, 0, lane);
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        half8 nxt[KB];
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb)
-          sacc[kb] = mfma32(RT::row_frag(st, kb * 32, kk, lane), qf[kk], sacc[kb]);
+          nxt[kb] = kk + 1 < KK ? RT::row_frag(st, kb * 32, kk + 1, lane) : kfr[kb];
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) sacc[kb] = mfma32(kfr[kb], qf[kk], sacc[kb]);
+        if (kk + 1 < KK) {
+          __builtin_amdgcn_sched_group_barrier(0x100, KB, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, KB, 0);
+        }
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) kfr[kb] = nxt[kb];
+      }
 
       // ---- mask (key > query, or key past S), row max ----
       if ((causal && key0 + BKV - 1 > qw0) || key0 + BKV > S) {   // wave-uniform
