@@ -190,7 +190,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
                 const lt_half* __restrict__ A, int64_t lda,
                 const lt_half* __restrict__ B, int64_t ldb, float beta,
                 const lt_half* R, int64_t ldr, lt_half* C, int64_t ldc, int tiles_m,
-                int tiles_n, int group_m, lt_half* X1, int64_t ldx1, int64_t F,
+                int tiles_n, int group_m, lt_half* X1, int64_t ldx1, int64_t Fb, int64_t P,
                 const lt_half* bias) {
   constexpr int NT = WGM * WGN * kWave;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;   // wave tile
@@ -230,7 +230,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   OB ob;
   oa.init(A, lda, m0, M, wave, lane);
   if constexpr (EPI == 1)
-    ob.init(B, ldb, n0, F, wave, lane, F);
+    ob.init(B, ldb, n0, Fb, wave, lane, P);
   else
     ob.init(B, ldb, n0, N, wave, lane);
 
@@ -352,7 +352,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
 #pragma unroll
       for (int j = 0; j < TN / 2; ++j) {
         const int64_t n = n0 + wn * (WTN / 2) + j * 16 + 4 * (lane >> 4);
-        if (n >= F) continue;
+        if (n >= Fb) continue;
         half4 g4, u4, a4;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -363,7 +363,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
           a4[e] = (_Float16)(g * sigmoid_f(g) * u);
         }
         *reinterpret_cast<half4*>(C + m * ldc + n) = g4;
-        *reinterpret_cast<half4*>(C + m * ldc + F + n) = u4;
+        *reinterpret_cast<half4*>(C + m * ldc + P + n) = u4;
         *reinterpret_cast<half4*>(X1 + m * ldx1 + n) = a4;
       }
     }
@@ -411,7 +411,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
           const int64_t nc = n < N ? n : N - 4;
           if constexpr (EPI == 2) {
             in[ii][j][0] = *reinterpret_cast<const half4*>(X1 + mc * ldx1 + nc);
-            in[ii][j][1] = *reinterpret_cast<const half4*>(X1 + mc * ldx1 + F + nc);
+            in[ii][j][1] = *reinterpret_cast<const half4*>(X1 + mc * ldx1 + P + nc);
           } else {
             in[ii][j][0] = *reinterpret_cast<const half4*>(R + mc * ldr + nc);
           }
@@ -459,7 +459,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
           const int64_t n = nb + j * 16;
           if (m < M && n < N) {
             *reinterpret_cast<half4*>(C + m * ldc + n) = out[ii][j][0];
-            if constexpr (EPI == 2) *reinterpret_cast<half4*>(C + m * ldc + F + n) = out[ii][j][1];
+            if constexpr (EPI == 2) *reinterpret_cast<half4*>(C + m * ldc + P + n) = out[ii][j][1];
           }
         }
       }
@@ -481,17 +481,88 @@ hipError_t launch(const GemmArgs& g, hipStream_t s) {
   hipLaunchKernelGGL((gemm_f16_kernel<BM, BN, WGM, WGN, BK, NS, TA, TB, EPI>),
                      dim3(tiles_m * tiles_n), dim3(WGM * WGN * kWave), 0, s, g.M, g.N, g.K, g.alpha,
                      g.A, g.lda, g.B, g.ldb, g.beta, g.R, g.ldr, g.C, g.ldc, tiles_m, tiles_n, 8,
-                     g.X1, g.ldx1, g.F, g.bias);
+                     g.X1, g.ldx1, g.F, g.pair_off > 0 ? g.pair_off : g.F, g.bias);
   return hipGetLastError();
+}
+
+// The same product restricted to output columns [n0, ...) (in units of
+// output columns; for the gate/up epilogue, of gate columns).
+template <bool TA, bool TB, int EPI>
+GemmArgs column_part(const GemmArgs& g, int64_t n0) {
+  GemmArgs t = g;
+  if (EPI == 1) {
+    t.pair_off = g.pair_off > 0 ? g.pair_off : g.F;
+    t.B = g.B + n0 * g.ldb;        // gate rows n0..; up rows stay pair_off further
+    t.F = g.F - n0;
+    t.N = 2 * t.F;
+    t.C = g.C + n0;
+    t.X1 = g.X1 + n0;
+  } else {
+    t.B = TB ? g.B + n0 * g.ldb : g.B + n0;
+    t.N = g.N - n0;
+    t.C = g.C + n0;
+    t.R = g.R + n0;
+    if (g.bias) t.bias = g.bias + n0;
+    if (EPI == 2) {
+      t.pair_off = g.pair_off > 0 ? g.pair_off : g.F;
+      t.X1 = g.X1 + n0;
+    }
+  }
+  return t;
+}
+
+// ... restricted to output rows [m0, ...).
+template <bool TA, bool TB, int EPI>
+GemmArgs row_part(const GemmArgs& g, int64_t m0) {
+  GemmArgs t = g;
+  t.A = TA ? g.A + m0 : g.A + m0 * g.lda;
+  t.M = g.M - m0;
+  t.C = g.C + m0 * g.ldc;
+  t.R = g.R + m0 * g.ldr;
+  if (EPI != 0) t.X1 = g.X1 + m0 * g.ldx1;
+  return t;
 }
 
 template <bool TA, bool TB, int EPI>
 hipError_t dispatch_tile(const GemmArgs& g, hipStream_t s) {
   // 256x256 tiles once there are about as many tiles as CUs; smaller
   // problems use 128x128 tiles so that more workgroups exist.
-  const int64_t big_tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
-  if (big_tiles >= 192) return launch<256, 256, 2, 4, 64, 2, TA, TB, EPI>(g, s);
-  return launch<128, 128, 2, 2, 64, 2, TA, TB, EPI>(g, s);
+  const int64_t unit_n = EPI == 1 ? 128 : 256;            // output columns per 256-wide tile
+  const int64_t ncols = EPI == 1 ? g.F : g.N;
+  const int64_t tm = (g.M + 255) / 256, tn = (ncols + unit_n - 1) / unit_n;
+  const int64_t big_tiles = tm * tn;
+  if (big_tiles < 192) return launch<128, 128, 2, 2, 64, 2, TA, TB, EPI>(g, s);
+  // A last wave at most half full runs as half-size tiles in one short round:
+  // whole waves of 256x256 tiles first, then the remaining columns (or rows)
+  // as 256x128 (or 128x256) tiles.
+  constexpr int64_t kCUs = 256;
+  const int64_t waves = big_tiles / kCUs, rem = big_tiles % kCUs;
+  if (waves >= 1 && rem > 0 && 2 * rem <= kCUs) {
+    const int64_t full = waves * kCUs;
+    if (full % tm == 0 && full / tm < tn) {
+      const int64_t n_main = (full / tm) * unit_n;
+      GemmArgs head = g;
+      if (EPI == 1) {
+        head.pair_off = g.pair_off > 0 ? g.pair_off : g.F;
+        head.F = n_main;
+        head.N = 2 * n_main;
+      } else {
+        head.N = n_main;
+      }
+      hipError_t e = launch<256, 256, 2, 4, 64, 2, TA, TB, EPI>(head, s);
+      if (e != hipSuccess) return e;
+      return launch<256, 128, 4, 2, 64, 2, TA, TB, EPI>(column_part<TA, TB, EPI>(g, n_main), s);
+    }
+    if (full % tn == 0 && full / tn < tm) {
+      const int64_t m_main = (full / tn) * 256;
+      GemmArgs head = g;
+      head.M = m_main;
+      hipError_t e = launch<256, 256, 2, 4, 64, 2, TA, TB, EPI>(head, s);
+      if (e != hipSuccess) return e;
+      return launch<128, 256, 2, 4, 64, 2, TA, TB, EPI>(row_part<TA, TB, EPI>(g, m_main), s);
+    }
+  }
+  return launch<256, 256, 2, 4, 64, 2, TA, TB, EPI>(g, s);
 }
 
 }  // namespace

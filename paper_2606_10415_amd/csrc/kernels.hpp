@@ -32,6 +32,9 @@ struct GemmArgs {
   int64_t F = 0;
   // optional bias [N] added to every row (epilogue 0 only)
   const lt_half* bias = nullptr;
+  // gate/up epilogues: distance between gate and up rows of B (1) / columns
+  // of C and X1 (1, 2); 0 means F (set for launches over part of the columns)
+  int64_t pair_off = 0;
 };
 
 struct AttnShape {

@@ -55,7 +55,11 @@ LAYOUTS = list(itertools.product([0, 1], [0, 1]))
 
 
 @pytest.mark.parametrize("transA,transB", LAYOUTS)
-@pytest.mark.parametrize("M,N,K", [(8, 8, 8), (136, 200, 72), (264, 520, 1000), (4096, 4096, 512)])
+@pytest.mark.parametrize("M,N,K", [(8, 8, 8), (136, 200, 72), (264, 520, 1000), (4096, 4096, 512),
+                                   # a last wave of at most half the CUs runs as half-size tiles:
+                                   # column split (8 x 34 tiles), row split (34 x 8), ragged edges
+                                   (2048, 8704, 256), (8704, 2048, 256), (2040, 8696, 264),
+                                   (8696, 2040, 264)])
 def test_gemm_exact_integers_bitwise(env, transA, transB, M, N, K):
     print(f"gemm exact ints trans=({transA},{transB}) M={M} N={N} K={K}", flush=True)
     a = uniform_int_f16(1, (M, K), -2, 2)

@@ -61,7 +61,11 @@ def test_swiglu_extreme_inputs(env):
 
 @pytest.mark.parametrize("T,H,F", [(272, 256, 344), (64, 128, 688), (8, 64, 8), (1000, 512, 1000),
                                    (4096, 4096, 11008), (2048, 5120, 13824),
-                                   (2040, 512, 5000)])
+                                   (2040, 512, 5000),
+                                   # half-size tail tiles: column split of both epilogues,
+                                   # row split of both, and ragged versions
+                                   (2048, 256, 8704), (8704, 256, 2048), (2040, 256, 8696),
+                                   (8696, 256, 2040)])
 def test_fused_gemm_swiglu_parity(env, T, H, F):
     print(f"fused gemm swiglu T={T} H={H} F={F}", flush=True)
     torch, lt = env
