@@ -119,24 +119,36 @@ struct Operand {
       // rows carry absolute offsets and explicit out-of-range offsets)
       const lt_half* b = PAIRED ? base + k0 : base + row0 * ld + k0;
       const uint32_t n = PAIRED ? nrec : nrec - (uint32_t)(k0 * 2);
+      if (kvalid >= BK) {
 #pragma unroll
-      for (int t = 0; t < PERW; ++t) {
-        const int i = wave * PERW + t;
-        uint32_t off = voff[t];
-        if (kvalid < BK) {
-          const int r = i * RPI + lane / CPR;
-          if (((lane % CPR) ^ swz(r)) * 8 >= kvalid) off = kOOB;
+        for (int t = 0; t < PERW; ++t) {
+          const int i = wave * PERW + t;
+          lds_dma16_opaque(b, n, lds + i * 1024, voff[t]);
         }
-        lds_dma16_opaque(b, n, lds + i * 1024, off);
+      } else {
+#pragma unroll
+        for (int t = 0; t < PERW; ++t) {
+          const int i = wave * PERW + t;
+          const int r = i * RPI + lane / CPR;
+          const uint32_t off = ((lane % CPR) ^ swz(r)) * 8 >= kvalid ? kOOB : voff[t];
+          lds_dma16_opaque(b, n, lds + i * 1024, off);
+        }
       }
     } else {
       const lt_half* b = base + k0 * ld + row0;
+      if (kvalid >= BK) {
 #pragma unroll
-      for (int t = 0; t < PERW; ++t) {
-        const int i = wave * PERW + t;
-        uint32_t off = voff[t];
-        if (kvalid < BK && i * KR_PER + lane / LPR >= kvalid) off = kOOB;
-        lds_dma16_opaque(b, nrec, lds + i * 1024, off);
+        for (int t = 0; t < PERW; ++t) {
+          const int i = wave * PERW + t;
+          lds_dma16_opaque(b, nrec, lds + i * 1024, voff[t]);
+        }
+      } else {
+#pragma unroll
+        for (int t = 0; t < PERW; ++t) {
+          const int i = wave * PERW + t;
+          const uint32_t off = i * KR_PER + lane / LPR >= kvalid ? kOOB : voff[t];
+          lds_dma16_opaque(b, nrec, lds + i * 1024, off);
+        }
       }
     }
   }
@@ -213,7 +225,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar addressing
   const int wm = wave / WGN;
   const int wn = wave % WGN;
 
