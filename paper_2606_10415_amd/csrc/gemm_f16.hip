@@ -208,13 +208,12 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   constexpr int WTM = BM / WGM, WTN = BN / WGN;   // wave tile
   constexpr int TM = WTM / 16, TN = WTN / 16;     // 16x16 MFMA blocks per wave
   static_assert(EPI != 1 || (TB && WTN == 64), "paired gate/up tiles: 32 + 32 columns per wave");
-  // Loader waves: for the NT and TN layouts of an 8-wave tile, only waves
-  // 0-3 (one per SIMD) issue the direct loads, twice as many each; the other
-  // four waves only compute.  Fewer waves feeding the shared load queues
-  // measured 4-12% faster there; for NN (and TT) all eight waves load, which
-  // measured faster for those layouts.
+  // Loader waves: in an 8-wave tile only waves 0-3 (one per SIMD) issue the
+  // direct loads, twice as many each; the other four waves only compute.
+  // Fewer waves feeding the shared load queues measured 4-13% faster in
+  // every layout.
   constexpr int NWAVE = NT / kWave;
-  constexpr int LOADERS = (NWAVE >= 8 && TA != TB) ? 4 : NWAVE;
+  constexpr int LOADERS = NWAVE >= 8 ? 4 : NWAVE;
   constexpr bool SPLIT_ISSUE = LOADERS < NWAVE;
   using OA = Operand<BM, BK, !TA, LOADERS * kWave>;
   using OB = Operand<BN, BK, TB, LOADERS * kWave, EPI == 1>;
