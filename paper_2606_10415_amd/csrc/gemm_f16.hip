@@ -284,12 +284,6 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
     if (s < nk) issue(s);
   wait_slices<PER_SLICE, NS - 1>(min(NS - 1, nk - 1));
   __syncthreads();
-  if (nk > 0) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i) fa[i] = oa.frag(smem, wm * WTM + i * 16, 0, lane);
-#pragma unroll
-    for (int j = 0; j < TN; ++j) fb[0][j] = ob.frag(smem + OA::BYTES, wn * WTN + j * 16, 0, lane);
-  }
 
   // One MFMA step on (fa, fb[S]).  With LD, the fragments of the next step
   // (32-wide k-step kk of stage st) are read meanwhile: after the MFMAs of A
@@ -305,6 +299,23 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   static_assert(TN <= TM || TN % TM == 0, "B fragments must spread over the A rows");
   constexpr int BPI = TN <= TM ? 1 : TN / TM;
   constexpr int NBI = TN <= TM ? TN : TM;
+  // First fragments, read in the order the steps read theirs (after A row i:
+  // the B fragments of row i, then A fragment i).  The LDS counter waits at
+  // the top of the slice loop then hold for the entry from here as well as
+  // for the loop's back edge; with all B fragments read last, the waits the
+  // compiler derived for the merged entry stalled each slice's first MFMAs
+  // on the reads of the previous step's last rows.
+  if (nk > 0) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      if (i < NBI) {
+#pragma unroll
+        for (int q = 0; q < BPI; ++q)
+          fb[0][i + q * TM] = ob.frag(smem + OA::BYTES, wn * WTN + (i + q * TM) * 16, 0, lane);
+      }
+      fa[i] = oa.frag(smem, wm * WTM + i * 16, 0, lane);
+    }
+  }
   auto step = [&](auto S_, auto LD_, const char* st, int kk, auto&& after_first_row) {
     constexpr int S = decltype(S_)::value;
     constexpr bool LD = decltype(LD_)::value;
