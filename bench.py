@@ -31,9 +31,11 @@ from paper_2606_10415_amd.synth import WORKLOADS, layer_inputs, norm_inputs  # n
 PEAK_FP16_TFLOPS = 2516.6     # MI355X dense FP16 MFMA (256 CU x 2.4 GHz x 4096 FLOP/clk)
 PEAK_HBM_GBS = 8000.0
 
-# HBM traffic of the GEMM kernel at llama2-7b: mean bytes per launch over the 12
-# GEMM launches of one layer step (the paper's layer, SwiGLU in the gate/up and
-# down-dgrad epilogues), from two rocprofv3 --pmc runs of this script
+# HBM traffic of the GEMM kernel at llama2-7b: mean bytes per GEMM call over the
+# 12 GEMM calls of one layer step (the paper's layer, SwiGLU in the gate/up and
+# down-dgrad epilogues; the gate/up forward and its weight gradient run as a
+# 256x256 dispatch plus a half-tile tail dispatch, counted together as their
+# call), from two rocprofv3 --pmc runs of this script
 # (FETCH_SIZE, then WRITE_SIZE, with --copy-calibration-mib 1024) each scaled by
 # what the same counter reads for the calibration copy of known size.  The
 # figure holds only for the kernel sources it was measured on: any change to
@@ -42,9 +44,9 @@ GEMM_TRAFFIC = {
     "workload": "llama2-7b",
     "layer": "paper",
     "fuse_swiglu": True,
-    "sources_sha256": "e464e457cd799d4db4173199118ef3dc57dc2125d3a7f640ee09c54fb2316475",
-    "fetch_bytes_per_launch": 687996275,
-    "write_bytes_per_launch": 95126881,
+    "sources_sha256": "e8a93b39156203b78b76947713ebd09fb2a3d9156740ff1908013f6da3e94ecb",
+    "fetch_bytes_per_launch": 660814673,
+    "write_bytes_per_launch": 95728833,
 }
 GEMM_SOURCES = ("paper_2606_10415_amd/csrc/gemm_f16.hip", "paper_2606_10415_amd/csrc/common.hpp")
 
