@@ -60,7 +60,7 @@ attn_fwd_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar addressing
   const int lrow = lane & 31;
   const int g = lane >> 5;
 
