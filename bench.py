@@ -371,7 +371,7 @@ def main():
                    "Hq": w.Hq, "Hkv": w.Hkv, "D": w.D, "F": w.F, "causal": True,
                    "flops_per_step": fl["total"], "parallelism": "single GPU"},
         "frac_of_peak": round(value / PEAK_FP16_TFLOPS, 4),
-        "roofline": {"bound": "mfma", "kernel": "gemm_f16 (12 launches per step, two with the SwiGLU epilogues)",
+        "roofline": {"bound": "mfma", "kernel": "gemm_f16 (12 GEMM calls per step, two with the SwiGLU epilogues; achieved and traffic are per call, the two gate/up calls each running a 256x256 and a half-tile tail launch)",
                      "achieved": round(gemm_tflops, 1), "peak": PEAK_FP16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK_FP16_TFLOPS, 4),
                      "traffic": gemm_traffic(w, args.layer, L.fuse_swiglu)},
