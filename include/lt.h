@@ -125,6 +125,35 @@ lt_status lt_gemm_f16_bias(int transA, int transB, int64_t M, int64_t N,
                            lt_stream stream);
 
 /*
+ * GEMM with residual, optional bias and a caller-owned workspace (Sec. 4.1's
+ * GEMM primitive, as lt_gemm_f16_bias with bias optional):
+ *
+ *     C[M,N] = alpha * op(A) op(B) + beta * R[M,N] (+ bias[N])
+ *
+ *   Same conventions and errors as lt_gemm_f16_res; bias may be NULL (no
+ *   bias), else [N] FP16, 16-byte aligned.  The workspace lets the kernel
+ *   split the reduction (K) of the tiles of a last, at most half full, wave
+ *   of output tiles over several workgroups: their FP32 partial sums go to
+ *   the workspace and are added in a fixed order (deterministic) before the
+ *   single rounding of C.  The result can differ from lt_gemm_f16_res in the
+ *   last bits of those tiles (another FP32 summation order).
+ *   workspace: device memory owned by the caller, 16-byte aligned (else
+ *   LT_ERR_UNSUPPORTED), of at least lt_gemm_f16_workspace_size(...) bytes
+ *   (else LT_ERR_WORKSPACE); its contents on entry do not matter and it is
+ *   in use until the stream reaches the end of the call.  NULL: no split
+ *   (the call is then lt_gemm_f16_res / lt_gemm_f16_bias).  Calls that may
+ *   run concurrently need separate workspaces.
+ */
+size_t lt_gemm_f16_workspace_size(int transA, int transB, int64_t M, int64_t N,
+                                  int64_t K);
+lt_status lt_gemm_f16_ws(int transA, int transB, int64_t M, int64_t N,
+                         int64_t K, float alpha, const lt_half* A, int64_t lda,
+                         const lt_half* B, int64_t ldb, float beta,
+                         const lt_half* R, int64_t ldr, const lt_half* bias,
+                         lt_half* C, int64_t ldc, void* workspace,
+                         size_t workspace_bytes, lt_stream stream);
+
+/*
  * Bias gradient of a linear layer: db[n] = sum over t < T of dY[t][n]
  * (dY row-major [T, N] with row stride lddy).  FP32 sums in a fixed order
  * (deterministic), one rounding to FP16.  The caller-owned workspace, of at

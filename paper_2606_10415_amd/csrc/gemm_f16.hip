@@ -222,6 +222,15 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   static_assert(NS >= 2 && (NS - 1) * PER_SLICE <= 63, "vmcnt range");
   __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
 
+  if constexpr (EPI == 3) {
+    // split-K unit blockIdx.y of gridDim.y: slices [y*kc, (y+1)*kc) of the
+    // reduction, as a product of its own over the offset operands
+    const int64_t kc = ((K + BK - 1) / BK + gridDim.y - 1) / gridDim.y;
+    const int64_t k0 = (int64_t)blockIdx.y * kc * BK;
+    A += TA ? k0 * lda : k0;
+    B += TB ? k0 : k0 * ldb;
+    K = K - k0 < kc * BK ? K - k0 : kc * BK;
+  }
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar addressing
@@ -385,7 +394,22 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
 
   // ---- epilogue ----
   // lane holds column m = ... + lane % 16 and rows n = ... + 4*(lane/16) + 0..3
-  if constexpr (EPI == 1) {
+  if constexpr (EPI == 3) {
+    // FP32 partial sums of this split, unscaled: W[split][m][n], ldc floats
+    // per row (C is the workspace)
+    float* W = reinterpret_cast<float*>(C) + (int64_t)blockIdx.y * M * ldc;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int64_t m = m0 + wm * WTM + i * 16 + (lane & 15);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int64_t n = n0 + wn * WTN + j * 16 + 4 * (lane >> 4);
+        if (m < M && n < N)
+          *reinterpret_cast<float4*>(W + m * ldc + n) =
+              make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+      }
+    }
+  } else if constexpr (EPI == 1) {
     // accumulator blocks j and j + TN/2 hold the gate and up columns of the
     // same n: GU[m][n] = G, GU[m][F + n] = U, A[m][n] = silu(G) U (from the
     // FP32 values, one rounding each)
@@ -519,11 +543,11 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
 }
 
 template <int BM, int BN, int WGM, int WGN, int BK, int NS, bool TA, bool TB, int EPI>
-hipError_t launch(const GemmArgs& g, hipStream_t s) {
+hipError_t launch(const GemmArgs& g, hipStream_t s, int splits = 1) {
   const int tiles_m = (int)((g.M + BM - 1) / BM);
   const int tiles_n = EPI == 1 ? (int)((g.F + BN / 2 - 1) / (BN / 2)) : (int)((g.N + BN - 1) / BN);
   hipLaunchKernelGGL((gemm_f16_kernel<BM, BN, WGM, WGN, BK, NS, TA, TB, EPI>),
-                     dim3(tiles_m * tiles_n), dim3(WGM * WGN * kWave), 0, s, g.M, g.N, g.K, g.alpha,
+                     dim3(tiles_m * tiles_n, splits), dim3(WGM * WGN * kWave), 0, s, g.M, g.N, g.K, g.alpha,
                      g.A, g.lda, g.B, g.ldb, g.beta, g.R, g.ldr, g.C, g.ldc, tiles_m, tiles_n, 8,
                      g.X1, g.ldx1, g.F, g.pair_off > 0 ? g.pair_off : g.F, g.bias);
   return hipGetLastError();
@@ -567,6 +591,44 @@ GemmArgs row_part(const GemmArgs& g, int64_t m0) {
   return t;
 }
 
+// C = alpha * sum_s W[s] + beta * R + bias over an Mt x Nt region, the
+// splits summed in ascending order; eight columns per thread (Nt % 8 == 0).
+__global__ void __launch_bounds__(256)
+splitk_reduce_kernel(const float* __restrict__ W, int S, int64_t Mt, int64_t Nt, float alpha,
+                     float beta, const lt_half* R, int64_t ldr, const lt_half* __restrict__ bias,
+                     lt_half* C, int64_t ldc) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t n8 = Nt / 8;
+  if (idx >= Mt * n8) return;
+  const int64_t m = idx / n8, n = (idx % n8) * 8;
+  float v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = 0.f;
+  for (int sp = 0; sp < S; ++sp) {
+    const float* w = W + ((int64_t)sp * Mt + m) * Nt + n;
+    const float4 a = *reinterpret_cast<const float4*>(w);
+    const float4 b = *reinterpret_cast<const float4*>(w + 4);
+    v[0] += a.x; v[1] += a.y; v[2] += a.z; v[3] += a.w;
+    v[4] += b.x; v[5] += b.y; v[6] += b.z; v[7] += b.w;
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] *= alpha;
+  if (beta != 0.f) {
+    const half8 r = as_half8(ld16(R + m * ldr + n));
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] += beta * (float)r[e];
+  }
+  if (bias) {
+    const half8 bb = as_half8(ld16(bias + n));
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] += (float)bb[e];
+  }
+  half8 o;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] = (_Float16)v[e];
+  *reinterpret_cast<half8*>(C + m * ldc + n) = o;
+}
+
 template <bool TA, bool TB, int EPI>
 hipError_t dispatch_tile(const GemmArgs& g, hipStream_t s) {
   // 256x256 tiles once there are about as many tiles as CUs; smaller
@@ -581,6 +643,37 @@ hipError_t dispatch_tile(const GemmArgs& g, hipStream_t s) {
   // as 256x128 (or 128x256) tiles.
   constexpr int64_t kCUs = 256;
   const int64_t waves = big_tiles / kCUs, rem = big_tiles % kCUs;
+  SplitTail st;
+  if constexpr (EPI == 0) {
+    if (g.ws != nullptr && gemm_splitk_tail(g.M, g.N, g.K, &st) &&
+        gemm_splitk_ws_bytes(g.M, g.N, g.K) <= g.ws_bytes) {
+      // The last wave as split-K 256x256 tiles: whole waves first (full K),
+      // then the remaining tiles' K split S ways (FP32 partials in the
+      // workspace), then the fixed-order sum with alpha, beta * R and bias.
+      GemmArgs head = g, tail;
+      if (st.columns) {
+        head.N = st.split_at;
+        tail = column_part<TA, TB, 0>(g, st.split_at);
+      } else {
+        head.M = st.split_at;
+        tail = row_part<TA, TB, 0>(g, st.split_at);
+      }
+      hipError_t e = launch<256, 256, 2, 4, 64, 2, TA, TB, 0>(head, s);
+      if (e != hipSuccess) return e;
+      GemmArgs part = tail;
+      part.C = reinterpret_cast<lt_half*>(g.ws);
+      part.ldc = st.Nt;
+      part.beta = 0.f;
+      part.bias = nullptr;
+      e = launch<256, 256, 2, 4, 64, 2, TA, TB, 3>(part, s, st.S);
+      if (e != hipSuccess) return e;
+      const int64_t threads = st.Mt * (st.Nt / 8);
+      hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
+                         s, g.ws, st.S, st.Mt, st.Nt, g.alpha, g.beta, tail.R, tail.ldr, tail.bias,
+                         tail.C, tail.ldc);
+      return hipGetLastError();
+    }
+  }
   if (waves >= 1 && rem > 0 && 2 * rem <= kCUs) {
     const int64_t full = waves * kCUs;
     if (full % tm == 0 && full / tm < tn) {
@@ -610,6 +703,44 @@ hipError_t dispatch_tile(const GemmArgs& g, hipStream_t s) {
 }
 
 }  // namespace
+
+bool gemm_splitk_tail(int64_t M, int64_t N, int64_t K, SplitTail* p) {
+  // the geometry of the half-tile tail (256x256 tiles, one wave = 256 CUs),
+  // with the last wave's K split so that its units fill about one wave
+  constexpr int64_t kCUs = 256, kMinSlices = 8, kMaxSplits = 8;
+  if (M <= 0 || N <= 0 || K <= 0) return false;
+  const int64_t tm = (M + 255) / 256, tn = (N + 255) / 256, tiles = tm * tn;
+  if (tiles < 192) return false;
+  const int64_t waves = tiles / kCUs, rem = tiles % kCUs;
+  if (waves < 1 || rem == 0 || 2 * rem > kCUs) return false;
+  const int64_t nk = (K + 63) / 64;
+  int64_t S = kCUs / rem;
+  if (S > kMaxSplits) S = kMaxSplits;
+  if (S > nk / kMinSlices) S = nk / kMinSlices;
+  if (S < 2) return false;
+  const int64_t full = waves * kCUs;
+  if (full % tm == 0 && full / tm < tn) {
+    p->columns = true;
+    p->split_at = (full / tm) * 256;
+    p->Mt = M;
+    p->Nt = N - p->split_at;
+  } else if (full % tn == 0 && full / tn < tm) {
+    p->columns = false;
+    p->split_at = (full / tn) * 256;
+    p->Mt = M - p->split_at;
+    p->Nt = N;
+  } else {
+    return false;
+  }
+  p->S = (int)S;
+  return true;
+}
+
+size_t gemm_splitk_ws_bytes(int64_t M, int64_t N, int64_t K) {
+  SplitTail p;
+  if (!gemm_splitk_tail(M, N, K, &p)) return 0;
+  return (size_t)p.S * (size_t)p.Mt * (size_t)p.Nt * sizeof(float);
+}
 
 hipError_t gemm_f16_launch(const GemmArgs& g, hipStream_t s) {
   if (g.epi == 1) return dispatch_tile<false, true, 1>(g, s);     // X Wgu^T

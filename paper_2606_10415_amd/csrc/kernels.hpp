@@ -35,7 +35,24 @@ struct GemmArgs {
   // gate/up epilogues: distance between gate and up rows of B (1) / columns
   // of C and X1 (1, 2); 0 means F (set for launches over part of the columns)
   int64_t pair_off = 0;
+  // optional FP32 workspace (epilogue 0): a last wave at most half full then
+  // runs with its K split (gemm_splitk_tail), when ws_bytes suffices
+  float* ws = nullptr;
+  size_t ws_bytes = 0;
 };
+
+// Split-K plan for the last, at most half full, wave of 256x256 tiles: the
+// tiles right of column split_at (columns) or below row split_at (rows), an
+// Mt x Nt region, computed as S partial products over K.  False: no split.
+struct SplitTail {
+  bool columns;
+  int64_t split_at;
+  int64_t Mt, Nt;
+  int S;
+};
+bool gemm_splitk_tail(int64_t M, int64_t N, int64_t K, SplitTail* p);
+// FP32 workspace bytes the split needs (0 when gemm_splitk_tail is false)
+size_t gemm_splitk_ws_bytes(int64_t M, int64_t N, int64_t K);
 
 struct AttnShape {
   int B, S, Hq, Hkv, D;

@@ -65,7 +65,8 @@ lt_status check_attn_common(const void* Q, const void* K, const void* V, int64_t
 static lt_status gemm_common(int transA, int transB, int64_t M, int64_t N, int64_t K, float alpha,
                              const lt_half* A, int64_t lda, const lt_half* B, int64_t ldb,
                              float beta, const lt_half* R, int64_t ldr, const lt_half* bias,
-                             lt_half* C, int64_t ldc, lt_stream stream) {
+                             lt_half* C, int64_t ldc, lt_stream stream,
+                             void* workspace = nullptr, size_t ws_bytes = 0) {
   if ((transA != 0 && transA != 1) || (transB != 0 && transB != 1))
     return fail(LT_ERR_INVALID_ARG, "transA/transB must be 0 or 1");
   if (M < 0 || N < 0 || K < 0) return fail(LT_ERR_INVALID_ARG, "negative GEMM size");
@@ -90,9 +91,16 @@ static lt_status gemm_common(int transA, int transB, int64_t M, int64_t N, int64
   if (lda >= ((int64_t)1 << 22) || ldb >= ((int64_t)1 << 22))
     return fail(LT_ERR_UNSUPPORTED, "lda/ldb must be < 2^22 elements (32-bit buffer offsets)");
   if (bias && !aligned16(bias)) return fail(LT_ERR_UNSUPPORTED, "bias must be 16-byte aligned");
+  if (workspace) {
+    const size_t need = K > 0 ? lt::gemm_splitk_ws_bytes(M, N, K) : 0;
+    if (ws_bytes < need) return fail(LT_ERR_WORKSPACE, "workspace needs %zu bytes", need);
+    if (!aligned16(workspace)) return fail(LT_ERR_UNSUPPORTED, "workspace must be 16-byte aligned");
+  }
   lt::GemmArgs g{transA, transB, M, N, K, alpha, beta, A, lda, B, ldb,
                  beta != 0.f ? R : C, beta != 0.f ? ldr : ldc, C, ldc};
   g.bias = bias;
+  g.ws = static_cast<float*>(workspace);
+  g.ws_bytes = workspace ? ws_bytes : 0;
   return from_hip(lt::gemm_f16_launch(g, reinterpret_cast<hipStream_t>(stream)), "gemm launch");
 }
 
@@ -128,6 +136,20 @@ lt_status lt_gemm_f16_bias(int transA, int transB, int64_t M, int64_t N, int64_t
   if (!bias && M > 0 && N > 0) return fail(LT_ERR_INVALID_ARG, "NULL bias");
   return gemm_common(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, R, ldr, bias, C, ldc,
                      stream);
+}
+
+size_t lt_gemm_f16_workspace_size(int transA, int transB, int64_t M, int64_t N, int64_t K) {
+  if ((transA != 0 && transA != 1) || (transB != 0 && transB != 1)) return 0;
+  if (M <= 0 || N <= 0 || K <= 0) return 0;
+  return lt::gemm_splitk_ws_bytes(M, N, K);
+}
+
+lt_status lt_gemm_f16_ws(int transA, int transB, int64_t M, int64_t N, int64_t K, float alpha,
+                         const lt_half* A, int64_t lda, const lt_half* B, int64_t ldb, float beta,
+                         const lt_half* R, int64_t ldr, const lt_half* bias, lt_half* C,
+                         int64_t ldc, void* workspace, size_t workspace_bytes, lt_stream stream) {
+  return gemm_common(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, R, ldr, bias, C, ldc,
+                     stream, workspace, workspace_bytes);
 }
 
 size_t lt_bias_grad_workspace_size(int64_t T, int64_t N) {

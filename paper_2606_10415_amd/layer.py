@@ -81,7 +81,8 @@ class DecoderLayer:
         self.Y = e(T, sh.H)
         # backward temporaries (shareable between the layers of a stage)
         if share_bwd is not None:
-            for k in ("dA", "dGU", "dH1", "dO", "dQKV", "dX", "ws", "ws_bytes"):
+            for k in ("dA", "dGU", "dH1", "dO", "dQKV", "dX", "ws", "ws_bytes", "gemm_ws",
+                      "gemm_ws_bytes"):
                 setattr(self, k, getattr(share_bwd, k))
         else:
             self.dA = e(T, sh.F)
@@ -92,6 +93,11 @@ class DecoderLayer:
             self.dX = e(T, sh.H)
             self.ws_bytes = lt.lt_attn_bwd_workspace_size(sh.B, sh.S, sh.Hq, sh.Hkv, sh.D)
             self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.dev)
+            # split-K workspace of the plain GEMM calls (one at a time on the stream)
+            self.gemm_ws_bytes = max(lt.lt_gemm_f16_workspace_size(ta, tb, M, N, K)
+                                     for _, ta, tb, M, N, K in self._gemm_calls())
+            self.gemm_ws = (torch.empty(self.gemm_ws_bytes, dtype=torch.uint8, device=self.dev)
+                            if self.gemm_ws_bytes else None)
         self.dWqkv = e(*self.Wqkv.shape)
         self.dWo = e(*self.Wo.shape)
         self.dWgu = e(*self.Wgu.shape)
@@ -123,6 +129,16 @@ class DecoderLayer:
             self.bias_ws = torch.empty(self.bias_ws_bytes, dtype=torch.uint8, device=self.dev)
 
     # ------------------------------------------------------------ steps
+    def _gemm(self, ta, tb, M, N, K, A, lda, B, ldb, beta, C, ldc, stream, R=None, ldr=None,
+              bias=None):
+        """C = op(A) op(B) + beta R (+ bias), R defaulting to C, with the layer's
+        split-K workspace (a last, at most half full, wave of output tiles
+        splits its K over several workgroups)."""
+        if R is None:
+            R, ldr = C, ldc
+        lt.lt_gemm_f16_ws(ta, tb, M, N, K, 1.0, A, lda, B, ldb, beta, R, ldr, bias, C, ldc,
+                          self.gemm_ws, self.gemm_ws_bytes, stream)
+
     def _attn_ptrs(self, base):
         p = base.data_ptr()
         return p, p + 2 * self.hd, p + 2 * (self.hd + self.sh.Hkv * self.sh.D)
@@ -138,11 +154,11 @@ class DecoderLayer:
             mark("rmsnorm1_fwd")
             xin = self.Xn
         if self.bqkv is not None:
-            lt.lt_gemm_f16_bias(0, 1, T, self.qkv, sh.H, 1.0, xin, sh.H, self.Wqkv, sh.H, 0.0, None,
-                                self.qkv, self.bqkv, self.QKV, self.qkv, stream)
+            self._gemm(0, 1, T, self.qkv, sh.H, xin, sh.H, self.Wqkv, sh.H, 0.0, self.QKV, self.qkv,
+                       stream, bias=self.bqkv)
         else:
-            lt.lt_gemm_f16(0, 1, T, self.qkv, sh.H, 1.0, xin, sh.H, self.Wqkv, sh.H, 0.0,
-                           self.QKV, self.qkv, stream)
+            self._gemm(0, 1, T, self.qkv, sh.H, xin, sh.H, self.Wqkv, sh.H, 0.0, self.QKV, self.qkv,
+                       stream)
         mark("qkv_fwd")
         if self.norm is not None:
             lt.lt_rope_f16(self.QKV, self.qkv, sh.B, sh.S, sh.Hq + sh.Hkv, sh.D, self.CS, 0, stream)
@@ -151,8 +167,8 @@ class DecoderLayer:
         lt.lt_attn_fwd(q, k, v, self.qkv, self.qkv, self.O, self.hd, self.LSE, sh.B, sh.S, sh.Hq,
                        sh.Hkv, sh.D, self.scale, 1, stream)
         mark("attn_fwd")
-        lt.lt_gemm_f16_res(0, 1, T, sh.H, self.hd, 1.0, self.O, self.hd, self.Wo, self.hd, 1.0,
-                           self.X, sh.H, self.H1, sh.H, stream)
+        self._gemm(0, 1, T, sh.H, self.hd, self.O, self.hd, self.Wo, self.hd, 1.0, self.H1, sh.H,
+                   stream, R=self.X, ldr=sh.H)
         mark("o_fwd")
         hin = self.H1
         if self.norm is not None:
@@ -165,13 +181,13 @@ class DecoderLayer:
                                      sh.H, sh.F, stream)
             mark("gu_fwd")
         else:
-            lt.lt_gemm_f16(0, 1, T, 2 * sh.F, sh.H, 1.0, hin, sh.H, self.Wgu, sh.H, 0.0, self.GU,
-                           2 * sh.F, stream)
+            self._gemm(0, 1, T, 2 * sh.F, sh.H, hin, sh.H, self.Wgu, sh.H, 0.0, self.GU, 2 * sh.F,
+                       stream)
             mark("gu_fwd")
             lt.lt_swiglu_fwd(self.GU, self.A, T, sh.F, stream)
             mark("swiglu_fwd")
-        lt.lt_gemm_f16_res(0, 1, T, sh.H, sh.F, 1.0, self.A, sh.F, self.Wd, sh.F, 1.0, self.H1,
-                           sh.H, self.Y, sh.H, stream)
+        self._gemm(0, 1, T, sh.H, sh.F, self.A, sh.F, self.Wd, sh.F, 1.0, self.Y, sh.H, stream,
+                   R=self.H1, ldr=sh.H)
         mark("down_fwd")
 
     def backward(self, stream=None, hook=None):
@@ -181,42 +197,41 @@ class DecoderLayer:
         if self.accumulate and (self.norm is not None or self.bqkv is not None):
             raise ValueError("gradient accumulation covers the four projection weights only")
         wb = 1.0 if self.accumulate else 0.0     # weight gradients: overwrite or accumulate
-        lt.lt_gemm_f16(1, 0, sh.H, sh.F, T, 1.0, self.dY, sh.H, self.A, sh.F, wb, self.dWd, sh.F,
-                       stream)
+        self._gemm(1, 0, sh.H, sh.F, T, self.dY, sh.H, self.A, sh.F, wb, self.dWd, sh.F, stream)
         mark("down_wgrad")
         if self.fuse_swiglu:
             lt.lt_gemm_swiglu_bwd_f16(self.dY, sh.H, self.Wd, sh.F, self.GU, 2 * sh.F, self.dGU,
                                       2 * sh.F, T, sh.H, sh.F, stream)
             mark("down_dgrad")
         else:
-            lt.lt_gemm_f16(0, 0, T, sh.F, sh.H, 1.0, self.dY, sh.H, self.Wd, sh.F, 0.0, self.dA,
-                           sh.F, stream)
+            self._gemm(0, 0, T, sh.F, sh.H, self.dY, sh.H, self.Wd, sh.F, 0.0, self.dA, sh.F,
+                       stream)
             mark("down_dgrad")
             lt.lt_swiglu_bwd(self.dA, self.GU, self.dGU, T, sh.F, stream)
             mark("swiglu_bwd")
         # gate/up projection
         hin = self.H1n if self.norm is not None else self.H1
-        lt.lt_gemm_f16(1, 0, 2 * sh.F, sh.H, T, 1.0, self.dGU, 2 * sh.F, hin, sh.H, wb,
-                       self.dWgu, sh.H, stream)
+        self._gemm(1, 0, 2 * sh.F, sh.H, T, self.dGU, 2 * sh.F, hin, sh.H, wb, self.dWgu, sh.H,
+                   stream)
         mark("gu_wgrad")
         if self.norm is not None:
-            lt.lt_gemm_f16(0, 0, T, sh.H, 2 * sh.F, 1.0, self.dGU, 2 * sh.F, self.Wgu, sh.H, 0.0,
-                           self.dH1n, sh.H, stream)
+            self._gemm(0, 0, T, sh.H, 2 * sh.F, self.dGU, 2 * sh.F, self.Wgu, sh.H, 0.0, self.dH1n,
+                       sh.H, stream)
             mark("gu_dgrad")
             lt.lt_rmsnorm_bwd(self.dH1n, sh.H, self.H1, sh.H, self.Wn2, self.rstd2, self.dY, sh.H,
                               self.dH1, sh.H, self.dWn2, self.rms_ws, self.rms_ws_bytes, T, sh.H,
                               stream)
             mark("rmsnorm2_bwd")
         else:
-            lt.lt_gemm_f16_res(0, 0, T, sh.H, 2 * sh.F, 1.0, self.dGU, 2 * sh.F, self.Wgu, sh.H,
-                               1.0, self.dY, sh.H, self.dH1, sh.H, stream)
+            self._gemm(0, 0, T, sh.H, 2 * sh.F, self.dGU, 2 * sh.F, self.Wgu, sh.H, 1.0, self.dH1,
+                       sh.H, stream, R=self.dY, ldr=sh.H)
             mark("gu_dgrad")
         # output projection
-        lt.lt_gemm_f16(1, 0, sh.H, self.hd, T, 1.0, self.dH1, sh.H, self.O, self.hd, wb, self.dWo,
-                       self.hd, stream)
+        self._gemm(1, 0, sh.H, self.hd, T, self.dH1, sh.H, self.O, self.hd, wb, self.dWo, self.hd,
+                   stream)
         mark("o_wgrad")
-        lt.lt_gemm_f16(0, 0, T, self.hd, sh.H, 1.0, self.dH1, sh.H, self.Wo, self.hd, 0.0, self.dO,
-                       self.hd, stream)
+        self._gemm(0, 0, T, self.hd, sh.H, self.dH1, sh.H, self.Wo, self.hd, 0.0, self.dO, self.hd,
+                   stream)
         mark("o_dgrad")
         # attention
         q, k, v = self._attn_ptrs(self.QKV)
@@ -234,25 +249,31 @@ class DecoderLayer:
             mark("qkv_bias_grad")
         # QKV projection
         xin = self.Xn if self.norm is not None else self.X
-        lt.lt_gemm_f16(1, 0, self.qkv, sh.H, T, 1.0, self.dQKV, self.qkv, xin, sh.H, wb,
-                       self.dWqkv, sh.H, stream)
+        self._gemm(1, 0, self.qkv, sh.H, T, self.dQKV, self.qkv, xin, sh.H, wb, self.dWqkv, sh.H,
+                   stream)
         mark("qkv_wgrad")
         if self.norm is not None:
-            lt.lt_gemm_f16(0, 0, T, sh.H, self.qkv, 1.0, self.dQKV, self.qkv, self.Wqkv, sh.H, 0.0,
-                           self.dXn, sh.H, stream)
+            self._gemm(0, 0, T, sh.H, self.qkv, self.dQKV, self.qkv, self.Wqkv, sh.H, 0.0, self.dXn,
+                       sh.H, stream)
             mark("qkv_dgrad")
             lt.lt_rmsnorm_bwd(self.dXn, sh.H, self.X, sh.H, self.Wn1, self.rstd1, self.dH1, sh.H,
                               self.dX, sh.H, self.dWn1, self.rms_ws, self.rms_ws_bytes, T, sh.H,
                               stream)
             mark("rmsnorm1_bwd")
         else:
-            lt.lt_gemm_f16_res(0, 0, T, sh.H, self.qkv, 1.0, self.dQKV, self.qkv, self.Wqkv, sh.H,
-                               1.0, self.dH1, sh.H, self.dX, sh.H, stream)
+            self._gemm(0, 0, T, sh.H, self.qkv, self.dQKV, self.qkv, self.Wqkv, sh.H, 1.0, self.dX,
+                       sh.H, stream, R=self.dH1, ldr=sh.H)
             mark("qkv_dgrad")
 
     def step(self, stream=None, hook=None):
         self.forward(stream, hook)
         self.backward(stream, hook)
+
+    # plain GEMM calls of one step as (name, transA, transB, M, N, K): forward
+    # NT, weight gradients TN, data gradients NN
+    def _gemm_calls(self):
+        lay = {"fwd": (0, 1), "wgrad": (1, 0), "dgrad": (0, 0)}
+        return [(n,) + lay[n.split("_")[1]] + (M, N, K) for n, M, N, K in self.gemm_shapes()]
 
     # GEMM launches of one step, in call order, as (name, M, N, K)
     def gemm_shapes(self):

@@ -89,6 +89,11 @@ _lib.lt_swiglu_bwd.argtypes = [_vp, _vp, _vp, _i64, _i64, _vp]
 _lib.lt_gemm_f16_bias.restype = _int
 _lib.lt_gemm_f16_bias.argtypes = [_int, _int, _i64, _i64, _i64, ctypes.c_float, _vp, _i64, _vp, _i64,
                                   ctypes.c_float, _vp, _i64, _vp, _vp, _i64, _vp]
+_lib.lt_gemm_f16_workspace_size.restype = _sz
+_lib.lt_gemm_f16_workspace_size.argtypes = [_int, _int, _i64, _i64, _i64]
+_lib.lt_gemm_f16_ws.restype = _int
+_lib.lt_gemm_f16_ws.argtypes = [_int, _int, _i64, _i64, _i64, ctypes.c_float, _vp, _i64, _vp, _i64,
+                                ctypes.c_float, _vp, _i64, _vp, _vp, _i64, _vp, _sz, _vp]
 _lib.lt_bias_grad_workspace_size.restype = ctypes.c_size_t
 _lib.lt_bias_grad_workspace_size.argtypes = [_i64, _i64]
 _lib.lt_bias_grad_f16.restype = _int
@@ -198,6 +203,18 @@ def lt_gemm_f16_bias(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, R, ld
                                  _ptr(A), int(lda), _ptr(B), int(ldb), float(beta), _ptr(R),
                                  int(ldr), _ptr(bias), _ptr(C), int(ldc), _stream(stream)),
            "lt_gemm_f16_bias")
+
+
+def lt_gemm_f16_workspace_size(transA, transB, M, N, K):
+    return int(_lib.lt_gemm_f16_workspace_size(int(transA), int(transB), int(M), int(N), int(K)))
+
+
+def lt_gemm_f16_ws(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, R, ldr, bias, C, ldc,
+                   workspace, ws_bytes, stream=None):
+    _check(_lib.lt_gemm_f16_ws(int(transA), int(transB), int(M), int(N), int(K), float(alpha),
+                               _ptr(A), int(lda), _ptr(B), int(ldb), float(beta), _ptr(R), int(ldr),
+                               _ptr(bias), _ptr(C), int(ldc), _ptr(workspace), int(ws_bytes),
+                               _stream(stream)), "lt_gemm_f16_ws")
 
 
 def lt_bias_grad_workspace_size(T, N):

@@ -16,7 +16,8 @@ def test_every_declared_symbol_is_exported():
             "lt_status_string", "lt_last_error", "lt_version", "lt_rmsnorm_fwd",
             "lt_rmsnorm_bwd", "lt_rmsnorm_bwd_workspace_size", "lt_rope_table",
             "lt_rope_f16", "lt_gemm_gu_swiglu_f16", "lt_gemm_swiglu_bwd_f16", "lt_gemm_f16_bias",
-            "lt_bias_grad_workspace_size", "lt_bias_grad_f16"} <= set(names)
+            "lt_bias_grad_workspace_size", "lt_bias_grad_f16", "lt_gemm_f16_workspace_size",
+            "lt_gemm_f16_ws"} <= set(names)
     for n in names:
         assert hasattr(lt._lib, n), f"{n} declared in lt.h but not exported"
 
@@ -288,3 +289,38 @@ def test_bias_grad_workspace_and_empty():
     assert lt.lt_bias_grad_workspace_size(4096, 7168) == 64 * 7168 * 4
     assert lt.lt_bias_grad_workspace_size(1, 8) % 256 == 0
     assert lt._lib.lt_bias_grad_f16(None, 0, 5, 0, None, None, 0, None) == lt.LT_OK
+
+
+# Split-K workspace of the last, at most half full, wave of 256x256 tiles (256 CUs):
+# S = min(256 // tail_tiles, 8, ceil(K/64) // 8) splits (none below 2), FP32 partials
+# over the tail region: S * Mt * Nt * 4 bytes.
+@pytest.mark.parametrize("M,N,K,want", [
+    (4096, 5120, 5120, 4 * 4096 * 1024 * 4),    # 16x20 tiles: 64 in the tail, columns 4096..5119
+    (5120, 4096, 4096, 4 * 1024 * 4096 * 4),    # 20x16 tiles: rows 4096..5119
+    (4096, 22016, 4096, 2 * 4096 * 1536 * 4),   # 16x86 tiles: 96 in the tail -> S = 2
+    (22016, 4096, 4096, 2 * 1536 * 4096 * 4),   # 86x16 tiles: rows 20480..22015
+    (4096, 5120, 1024, 2 * 4096 * 1024 * 4),    # 16 K-slices -> S = 2
+    (4096, 5120, 512, 0),                       # 8 K-slices: too few to split
+    (4096, 4096, 4096, 0),                      # whole waves only
+    (4096, 7168, 5120, 0),                      # 448 tiles: last wave 3/4 full
+    (1024, 1024, 8192, 0),                      # 16 tiles: 128x128 tiles, no tail
+    (0, 5120, 5120, 0), (4096, 5120, 0, 0),
+])
+def test_gemm_workspace_size(M, N, K, want):
+    for ta, tb in ((0, 1), (0, 0), (1, 0), (1, 1)):
+        assert lt.lt_gemm_f16_workspace_size(ta, tb, M, N, K) == want
+
+
+def _gemm_ws(ws, ws_bytes, M=4096, N=5120, K=5120):
+    return lt._lib.lt_gemm_f16_ws(0, 1, M, N, K, 1.0, FAKE, K, FAKE, K, 0.0, None, N, None, FAKE, N,
+                                  ws, ws_bytes, None)
+
+
+def test_gemm_ws_rejects_on_host():
+    need = lt.lt_gemm_f16_workspace_size(0, 1, 4096, 5120, 5120)
+    assert _gemm_ws(FAKE, need - 16) == lt.LT_ERR_WORKSPACE
+    assert _gemm_ws(FAKE + 8, need) == lt.LT_ERR_UNSUPPORTED
+    assert lt._lib.lt_gemm_f16_ws(2, 1, 64, 64, 64, 1.0, FAKE, 64, FAKE, 64, 0.0, None, 64, None, FAKE,
+                                  64, FAKE, 1 << 20, None) == lt.LT_ERR_INVALID_ARG
+    assert lt._lib.lt_gemm_f16_ws(0, 1, 64, 64, 64, 1.0, FAKE, 64, FAKE, 64, 0.0, None, 64, FAKE + 2,
+                                  FAKE, 64, None, 0, None) == lt.LT_ERR_UNSUPPORTED

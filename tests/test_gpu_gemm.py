@@ -138,3 +138,64 @@ def test_gemm_full_size_sampled(env, name, transA, transB, M, N, K):
     ref = oracle.gemm_entries(transA, transB, 1.0, a_np, b_np, 0.0, None, rows, cols)
     got = C.cpu().numpy()[rows, cols]
     assert rel_f(got, ref) <= 5e-3
+
+
+# ---- lt_gemm_f16_ws: the last, at most half full, wave of 256x256 tiles with its
+# K split over several workgroups (FP32 partials in the caller's workspace) ----
+
+def _run_ws(env, transA, transB, M, N, K, alpha, a, b, beta, r, bias=None, inplace=False):
+    torch, lt = env
+    A = torch.from_numpy(_stored(a, transA)).cuda()
+    B = torch.from_numpy(_stored(b, transB)).cuda()
+    R = torch.from_numpy(np.ascontiguousarray(r)).cuda()
+    C = R if inplace else torch.full((M, N), float("nan"), dtype=torch.float16, device="cuda")
+    Bias = None if bias is None else torch.from_numpy(bias).cuda()
+    need = lt.lt_gemm_f16_workspace_size(transA, transB, M, N, K)
+    assert need > 0, "shape must take the split-K tail"
+    ws = torch.full((need // 4,), float("nan"), dtype=torch.float32, device="cuda")   # contents unused
+    lt.lt_gemm_f16_ws(transA, transB, M, N, K, alpha, A, A.shape[1], B, B.shape[1], beta, R, N,
+                      Bias, C, N, ws, need)
+    torch.cuda.synchronize()
+    return C.cpu().numpy()
+
+
+def _tail_rows(M, n=40, seed=3):
+    rng = np.random.default_rng(seed)
+    return np.unique(np.concatenate([rng.choice(M, n, replace=False),
+                                     [0, 4095, 4096, M - 1] if M > 4096 else [0, M - 1]]))
+
+
+@pytest.mark.parametrize("transA,transB", LAYOUTS)
+@pytest.mark.parametrize("M,N,K,bias,inplace", [
+    (4096, 5120, 2048, False, False),   # column tail (columns 4096..), S = 4
+    (5120, 4096, 1024, True, False),    # row tail (rows 4096..), S = 2, bias
+    (4088, 5112, 1000, False, True),    # ragged M/N/K, ragged last split, C = R in place
+])
+def test_gemm_ws_split_tail_exact_integers(env, transA, transB, M, N, K, bias, inplace):
+    """Integer-valued inputs keep every FP32 partial and sum exact, so the split
+    result equals RNE(oracle) bit for bit on sampled rows of head and tail."""
+    print(f"gemm ws split tail trans=({transA},{transB}) M={M} N={N} K={K}", flush=True)
+    a = uniform_int_f16(21, (M, K), -2, 2)
+    b = uniform_int_f16(22, (K, N), -2, 2)
+    r = uniform_int_f16(23, (M, N), -8, 8)
+    bv = uniform_int_f16(24, (N,), -4, 4) if bias else None
+    got = _run_ws(env, transA, transB, M, N, K, 3.0, a, b, -2.0, r, bv, inplace)
+    rows = _tail_rows(M)
+    ref = oracle.gemm(0, 0, 3.0, a[rows], b, -2.0, r[rows])
+    if bias:
+        ref = ref + bv.astype(np.float64)
+    assert np.array_equal(got[rows].view(np.uint16), ref.astype(np.float16).view(np.uint16))
+
+
+@pytest.mark.parametrize("transA,transB", LAYOUTS)
+def test_gemm_ws_split_tail_normal_parity(env, transA, transB):
+    M, N, K = 4096, 5120, 5120
+    print(f"gemm ws split tail normal trans=({transA},{transB})", flush=True)
+    a = normal_f16(31, (M, K))
+    b = normal_f16(32, (K, N), 0.02)
+    r = normal_f16(33, (M, N))
+    got = _run_ws(env, transA, transB, M, N, K, 1.0, a, b, 1.0, r)
+    rows = _tail_rows(M, 24)
+    ref = oracle.gemm(0, 0, 1.0, a[rows], b, 1.0, r[rows])
+    assert rel_f(got[rows], ref) <= 5e-3
+    assert rel_f(got[rows][:, 4096:], ref[:, 4096:]) <= 5e-3      # the split columns alone
