@@ -33,9 +33,10 @@ PEAK_HBM_GBS = 8000.0
 
 # HBM traffic of the GEMM kernel at llama2-7b: mean bytes per GEMM call over the
 # 12 GEMM calls of one layer step (the paper's layer, SwiGLU in the gate/up and
-# down-dgrad epilogues; the gate/up forward and its weight gradient run as a
-# 256x256 dispatch plus a half-tile tail dispatch, counted together as their
-# call), from two rocprofv3 --pmc runs of this script
+# down-dgrad epilogues; the gate/up forward runs as a 256x256 dispatch plus a
+# half-tile tail dispatch, its weight gradient as a 256x256 dispatch, split-K
+# partials of its last wave and their reduction, all counted as their call),
+# from two rocprofv3 --pmc runs of this script
 # (FETCH_SIZE, then WRITE_SIZE, with --copy-calibration-mib 1024) each scaled by
 # what the same counter reads for the calibration copy of known size.  The
 # figure holds only for the kernel sources it was measured on: any change to
@@ -44,9 +45,9 @@ GEMM_TRAFFIC = {
     "workload": "llama2-7b",
     "layer": "paper",
     "fuse_swiglu": True,
-    "sources_sha256": "e8a93b39156203b78b76947713ebd09fb2a3d9156740ff1908013f6da3e94ecb",
-    "fetch_bytes_per_launch": 660814673,
-    "write_bytes_per_launch": 95728833,
+    "sources_sha256": "e0e50741fb4a999b41726cc5d2e211a314738ca5e9301b9bebc3a3ad42c53ed9",
+    "fetch_bytes_per_launch": 665281758,
+    "write_bytes_per_launch": 100094912,
 }
 GEMM_SOURCES = ("paper_2606_10415_amd/csrc/gemm_f16.hip", "paper_2606_10415_amd/csrc/common.hpp")
 
@@ -371,7 +372,7 @@ def main():
                    "Hq": w.Hq, "Hkv": w.Hkv, "D": w.D, "F": w.F, "causal": True,
                    "flops_per_step": fl["total"], "parallelism": "single GPU"},
         "frac_of_peak": round(value / PEAK_FP16_TFLOPS, 4),
-        "roofline": {"bound": "mfma", "kernel": "gemm_f16 (12 GEMM calls per step, two with the SwiGLU epilogues; achieved and traffic are per call, the two gate/up calls each running a 256x256 and a half-tile tail launch)",
+        "roofline": {"bound": "mfma", "kernel": "gemm_f16 (12 GEMM calls per step, two with the SwiGLU epilogues; achieved and traffic are per call; the gate/up forward adds a half-tile tail launch, the gate/up weight gradient a split-K last wave and its reduction)",
                      "achieved": round(gemm_tflops, 1), "peak": PEAK_FP16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(gemm_tflops / PEAK_FP16_TFLOPS, 4),
                      "traffic": gemm_traffic(w, args.layer, L.fuse_swiglu)},
