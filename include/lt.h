@@ -21,6 +21,10 @@
  *   - Every call is asynchronous on `stream` (NULL = the default stream).
  *     Argument checks run on the host before any launch; a non-LT_OK return
  *     means nothing was launched, except LT_ERR_HIP (a launch failed).
+ *   - Calls only launch kernels on `stream`: no allocation, memset, copy or
+ *     synchronisation, so a sequence of calls may be captured into a HIP
+ *     graph and replayed (the buffers, workspaces included, must then stay
+ *     allocated for the graph's lifetime).
  *   - Inputs must not alias outputs (the GEMM's C is both).
  *   - Float16 outputs are rounded once, round-to-nearest-even, from the
  *     FP32 accumulator; FP16 subnormals are kept.
