@@ -103,15 +103,30 @@ class ModelProfile:
         """Checkpoint of one layer: its input X."""
         return 2 * b * S * self.H
 
+    def gemm_workspace(self, b, S):
+        """FP32 split-K workspace of the layer's GEMMs (the largest any of its 12
+        GEMM shapes asks the library for; one at a time on the stream)."""
+        from . import lt
+        T, Hd = b * S, self.Hq * self.D
+        shapes = [(T, self.qkv_cols, self.H), (T, self.H, Hd), (T, 2 * self.F, self.H),
+                  (T, self.H, self.F), (self.H, self.F, T), (T, self.F, self.H),
+                  (2 * self.F, self.H, T), (T, self.H, 2 * self.F), (self.H, Hd, T),
+                  (T, Hd, self.H), (self.qkv_cols, self.H, T), (T, self.H, self.qkv_cols)]
+        return max(lt.lt_gemm_f16_workspace_size(0, 0, M, N, K) for M, N, K in shapes)
+
     def bwd_work(self, b, S):
         """Short-lived buffers of one layer's backward, shared by a stage's
         layers: dA, dGU, dH1, dO, dQKV, two input-gradient buffers (a layer
         reads one and writes the other), with norms the two normed-input
-        gradients, and the attention workspace (D and the base-2 LSE, FP32)."""
+        gradients, the attention workspace (D and the base-2 LSE, FP32, plus
+        FP32 partial dK, dV when a GQA group's query heads are split over
+        several workgroups) and the GEMMs' split-K workspace."""
         T = b * S
         half = T * (self.F + 2 * self.F + self.H + self.Hq * self.D + self.qkv_cols + 2 * self.H
                     + (2 * self.H if self.norm else 0))
-        return 2 * half + 2 * 4 * b * self.Hq * S
+        from . import lt
+        attn_ws = lt.lt_attn_bwd_workspace_size(b, S, self.Hq, self.Hkv, self.D)
+        return 2 * half + attn_ws + self.gemm_workspace(b, S)
 
 
 MODELS = {
