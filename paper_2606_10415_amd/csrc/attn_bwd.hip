@@ -221,6 +221,7 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
       half8 fq = RT::row_frag(qs, hq * 32, 0, lane);
       half8 fd = RT::row_frag(dos, hq * 32, 0, lane);
       half8 fv = RT::row_frag(smem + SM::V_OFF, wave * 32, 0, lane);
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
         half8 nq = fq, nd = fd, nv = fv;
@@ -240,6 +241,7 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
         fv = nv;
       }
 
+      __builtin_amdgcn_s_setprio(0);
       float p[16], ds[16];
 #pragma unroll
       for (int rq = 0; rq < 4; ++rq) {
@@ -274,6 +276,7 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
         pds[kc] = pack8(ds[8 * kc], ds[8 * kc + 1], ds[8 * kc + 2], ds[8 * kc + 3],
                         ds[8 * kc + 4], ds[8 * kc + 5], ds[8 * kc + 6], ds[8 * kc + 7]);
       }
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
@@ -283,6 +286,7 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
           dkacc[db] = mfma32(RT::template tr_frag<true>(qs, hq * 32 + kc * 16, db * 32, lane),
                              pds[kc], dkacc[db]);
         }
+      __builtin_amdgcn_s_setprio(0);
     }
     }
 
