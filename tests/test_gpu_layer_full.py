@@ -1,12 +1,14 @@
 """Full-size decoder layer in the launch configuration the benchmark times.
 
 One fwd+bwd step of ``DecoderLayer`` (fused SwiGLU, the layer's default) at the
-LLaMA-2-7B (MHA) and Qwen2.5-32B (GQA 5:1) shapes, B = 1, S = 4096.  Every step
+LLaMA-2-7B (MHA), Baichuan2-13B (MHA), Qwen2.5-32B (GQA 5:1) and LLaMA-2-70B
+(GQA 8:1, two sequences) shapes, S = 4096.  Every step
 of the layer is checked against the float64 oracle on outputs the oracle can
 compute one by one, taking that step's inputs from the GPU's own buffers:
 sampled rows of each activation / input-gradient product, sampled entries of
 each weight gradient (full-length dot products over the T tokens), and whole
-attention heads (forward O and LSE, backward dQ, dK, dV) for sampled heads.
+attention heads (forward O and LSE, backward dQ, dK, dV) for sampled heads of the
+last sequence of the micro-batch.
 
 Bars: relative Frobenius error <= 5e-3 for GEMM outputs, SwiGLU outputs and
 attention O; <= 1e-2 for dQ, dK, dV; LSE absolute error <= 1e-4.
@@ -22,7 +24,8 @@ from conftest import rel_f
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("name,heads", [("llama2-7b", (0, 31)), ("qwen2.5-32b", (7, 33))])
+@pytest.mark.parametrize("name,heads", [("llama2-7b", (0, 31)), ("baichuan2-13b", (3, 39)),
+                                        ("qwen2.5-32b", (7, 33)), ("llama2-70b", (9, 62))])
 def test_full_size_layer_step_sampled(name, heads):
     import torch
     assert torch.cuda.is_available(), "GPU tests need a ROCm device"
@@ -35,6 +38,8 @@ def test_full_size_layer_step_sampled(name, heads):
     torch.cuda.synchronize()
     c = lambda t: t.cpu().numpy()
     T, H, F, D = w.T, w.H, w.F, w.D
+    S, bi = w.S, w.B - 1                               # attention: the last sequence
+    seq = slice(bi * S, (bi + 1) * S)
     qd, kd = w.Hq * D, w.Hkv * D
     rng = np.random.default_rng(99)
     rows = np.unique(np.concatenate([rng.choice(T, 14, replace=False), [0, 1, T - 1]]))
@@ -54,31 +59,31 @@ def test_full_size_layer_step_sampled(name, heads):
     g = w.Hq // w.Hkv
     for h in heads:
         kv = h // g
-        q = QKV[:, h * D:(h + 1) * D]
-        k = QKV[:, qd + kv * D:qd + (kv + 1) * D]
-        v = QKV[:, qd + kd + kv * D:qd + kd + (kv + 1) * D]
+        q = QKV[seq, h * D:(h + 1) * D]
+        k = QKV[seq, qd + kv * D:qd + (kv + 1) * D]
+        v = QKV[seq, qd + kd + kv * D:qd + kd + (kv + 1) * D]
         o, lse, _ = oracle.attn_head_fwd(q, k, v, scale, causal=True)
-        err[f"O[h{h}]"] = rel_f(O[:, h * D:(h + 1) * D], o)
-        lse_err = float(np.max(np.abs(LSE[0, h] - lse)))
+        err[f"O[h{h}]"] = rel_f(O[seq, h * D:(h + 1) * D], o)
+        lse_err = float(np.max(np.abs(LSE[bi, h] - lse)))
         assert lse_err <= 1e-4, (h, lse_err)
-        gr = oracle.attn_head_bwd(q, k, v, dO[:, h * D:(h + 1) * D], scale, causal=True)
-        err[f"dQ[h{h}]"] = rel_f(dQKV[:, h * D:(h + 1) * D], gr["dq"])
+        gr = oracle.attn_head_bwd(q, k, v, dO[seq, h * D:(h + 1) * D], scale, causal=True)
+        err[f"dQ[h{h}]"] = rel_f(dQKV[seq, h * D:(h + 1) * D], gr["dq"])
         if g == 1:     # MHA: dK, dV of this kv head come from this query head alone
-            err[f"dK[h{h}]"] = rel_f(dQKV[:, qd + kv * D:qd + (kv + 1) * D], gr["dk"])
-            err[f"dV[h{h}]"] = rel_f(dQKV[:, qd + kd + kv * D:qd + kd + (kv + 1) * D], gr["dv"])
+            err[f"dK[h{h}]"] = rel_f(dQKV[seq, qd + kv * D:qd + (kv + 1) * D], gr["dk"])
+            err[f"dV[h{h}]"] = rel_f(dQKV[seq, qd + kd + kv * D:qd + kd + (kv + 1) * D], gr["dv"])
     if g > 1:          # GQA: the kv head's gradient sums its g query heads
         kv = heads[0] // g
-        k = QKV[:, qd + kv * D:qd + (kv + 1) * D]
-        v = QKV[:, qd + kd + kv * D:qd + kd + (kv + 1) * D]
-        dk = np.zeros((T, D))
-        dv = np.zeros((T, D))
+        k = QKV[seq, qd + kv * D:qd + (kv + 1) * D]
+        v = QKV[seq, qd + kd + kv * D:qd + kd + (kv + 1) * D]
+        dk = np.zeros((S, D))
+        dv = np.zeros((S, D))
         for h in range(kv * g, (kv + 1) * g):
-            gr = oracle.attn_head_bwd(QKV[:, h * D:(h + 1) * D], k, v, dO[:, h * D:(h + 1) * D],
+            gr = oracle.attn_head_bwd(QKV[seq, h * D:(h + 1) * D], k, v, dO[seq, h * D:(h + 1) * D],
                                       scale, causal=True)
             dk += gr["dk"]
             dv += gr["dv"]
-        err[f"dK[kv{kv}]"] = rel_f(dQKV[:, qd + kv * D:qd + (kv + 1) * D], dk)
-        err[f"dV[kv{kv}]"] = rel_f(dQKV[:, qd + kd + kv * D:qd + kd + (kv + 1) * D], dv)
+        err[f"dK[kv{kv}]"] = rel_f(dQKV[seq, qd + kv * D:qd + (kv + 1) * D], dk)
+        err[f"dV[kv{kv}]"] = rel_f(dQKV[seq, qd + kd + kv * D:qd + kd + (kv + 1) * D], dv)
     err["H1"] = rel_f(H1[rows], oracle.gemm(0, 1, 1.0, O[rows], p["Wo"], 1.0, X[rows]))
     gu = oracle.gemm(0, 1, 1.0, H1[rows], p["Wgu"])
     err["GU"] = rel_f(GU[rows], gu)
