@@ -13,7 +13,9 @@
 //     HBM -> LDS with direct buffer loads (16 B per lane, no register
 //     staging), issued one slice ahead so that they overlap the current
 //     slice's MFMA work -- the overlap of operand preparation with MACs that
-//     the paper's micro-kernel pipeline provides;
+//     the paper's micro-kernel pipeline provides.  In 8-wave tiles only one
+//     wave per SIMD issues them ("loader waves"), with uniform (scalar)
+//     addressing;
 //   * each operand keeps its HBM orientation in LDS.  A K-contiguous operand
 //     (forward A and B, dgrad A) is stored row-major; an M/N-contiguous one
 //     (dgrad B, wgrad A and B) is stored k-major and read with the gfx950
@@ -26,6 +28,11 @@
 //     grouped eight tile-rows at a time for L2 reuse of A and B.
 //   Buffer loads return zeros out of range, which provides the M, N and K
 //   tails without branches.
+//   A last wave of 256x256 tiles at most half full runs either as half-size
+//   tiles (256x128 / 128x256) or, when the caller provides an FP32 workspace,
+//   as 256x256 tiles whose K is split over several workgroups (epilogue 3
+//   stores their partial sums; splitk_reduce_kernel adds them in a fixed
+//   order and applies alpha, beta * R and the bias).
 #include <type_traits>
 
 #include "common.hpp"
