@@ -45,9 +45,9 @@ GEMM_TRAFFIC = {
     "workload": "llama2-7b",
     "layer": "paper",
     "fuse_swiglu": True,
-    "sources_sha256": "e0e50741fb4a999b41726cc5d2e211a314738ca5e9301b9bebc3a3ad42c53ed9",
-    "fetch_bytes_per_launch": 665281758,
-    "write_bytes_per_launch": 100094912,
+    "sources_sha256": "2ef160f073b004ca13455e5ef51f98d96eba678db8c067e897fd91c9d82a4ea8",
+    "fetch_bytes_per_launch": 664574840,
+    "write_bytes_per_launch": 100061412,
 }
 GEMM_SOURCES = ("paper_2606_10415_amd/csrc/gemm_f16.hip", "paper_2606_10415_amd/csrc/common.hpp")
 
