@@ -115,7 +115,7 @@ inline size_t attn_bwd_part_bytes(int B, int S, int Hq, int Hkv, int D) {
 }
 
 // RMSNorm backward (norm_rope.hip).  dW partial sums: one FP32 row of H per
-// wave, 4 waves per workgroup, rmsnorm_bwd_blocks(T) workgroups.
+// workgroup (8 waves), rmsnorm_bwd_blocks(T) workgroups.
 struct RmsBwdArgs {
   const lt_half* dY;
   int64_t lddy;
@@ -131,12 +131,13 @@ struct RmsBwdArgs {
   float* part;           // workspace
   int64_t T, H;
 };
-inline int rmsnorm_bwd_blocks(int64_t T) {
-  const int64_t b = (T + 15) / 16;
-  return (int)(b < 256 ? (b < 1 ? 1 : b) : 256);
+constexpr int kRmsBwdWaves = 8;
+inline int rmsnorm_bwd_blocks(int64_t T) {   // about one row per wave, at most 512 workgroups
+  const int64_t b = (T + kRmsBwdWaves - 1) / kRmsBwdWaves;
+  return (int)(b < 512 ? (b < 1 ? 1 : b) : 512);
 }
 inline size_t rmsnorm_bwd_ws_bytes(int64_t T, int64_t H) {
-  return align256((size_t)rmsnorm_bwd_blocks(T) * 4 * H * sizeof(float));
+  return align256((size_t)rmsnorm_bwd_blocks(T) * H * sizeof(float));
 }
 
 // bias gradient (column sum): FP32 partial rows of the workspace

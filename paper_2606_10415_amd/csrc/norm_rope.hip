@@ -6,13 +6,16 @@
 //     l, l + 64, ... of the row (coalesced), the sum of squares is a wave
 //     shuffle reduction; writes y = w * x * r (one rounding) and r.
 //       r = (mean_j x_j^2 + eps)^(-1/2)
-//   * rmsnorm_bwd: the same row layout; per row (two passes over the row,
-//     the second from L2)
+//   * rmsnorm_bwd: the same row layout, 8 waves per workgroup, about one row
+//     per wave; per row
 //       dx = r * w * g - r^3 * x / H * sum_j g_j w_j x_j   (+ residual R)
-//     and every wave keeps the FP32 partial of dw = sum_rows g * x * r for
-//     its own columns over the rows it visits; the partials go to the
-//     workspace and rmsnorm_dw_sum adds them in a fixed order
-//     (deterministic, no atomics).
+//     with g and x held in registers between the row dot product and dx
+//     (rows up to 6144 columns; wider rows are read twice, the second time
+//     from L2).  Every wave keeps the FP32 partial of dw = sum_rows g * x * r
+//     for the rows it visits; the workgroup adds its waves' partials in wave
+//     order through LDS, writes one partial row to the workspace, and
+//     rmsnorm_dw_sum adds those rows in a fixed order (deterministic, no
+//     atomics).
 //   * rope_table: cos / sin of p * base^(-2i/D) for p < S, i < D/2, with the
 //     angle formed and reduced in FP64 (positions up to 10^4 and more keep
 //     full FP32 accuracy), stored as FP32 pairs.
@@ -72,15 +75,20 @@ rmsnorm_fwd_kernel(const lt_half* __restrict__ X, int64_t ldx, const lt_half* __
 }
 
 // ---------------------------------------------------------------- backward
-// Workgroup = 4 waves over a contiguous range of rows; wave w takes rows
-// row0 + w, row0 + w + 4, ...; its dw partial goes to partial row
-// blockIdx.x * 4 + w of the workspace [nparts][H] FP32.
-template <int MAXK>
-__global__ void __launch_bounds__(64 * kRowsPerWg)
+// Workgroup = kBwdWaves waves over a contiguous range of rows; wave w takes
+// rows row0 + w, row0 + w + kBwdWaves, ...  Every wave accumulates its dw
+// partial for all columns in registers; at the end the workgroup adds its
+// waves' partials in wave order through LDS (8 columns per lane at a time)
+// and writes one partial row, blockIdx.x, of the workspace [nblk][H] FP32.
+constexpr int kBwdWaves = kRmsBwdWaves;
+
+template <int MAXK, bool ONEPASS>
+__global__ void __launch_bounds__(64 * kBwdWaves)
 rmsnorm_bwd_kernel(const lt_half* __restrict__ dY, int64_t lddy, const lt_half* __restrict__ X,
                    int64_t ldx, const lt_half* __restrict__ W, const float* __restrict__ RSTD,
                    const lt_half* __restrict__ R, int64_t ldr, lt_half* __restrict__ dX,
                    int64_t lddx, float* __restrict__ part, int64_t T, int H, int rows_per_wg) {
+  __shared__ float red[kBwdWaves][64 * 8];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int nch = H / 8;
@@ -94,22 +102,28 @@ rmsnorm_bwd_kernel(const lt_half* __restrict__ dY, int64_t lddy, const lt_half* 
 #pragma unroll
     for (int e = 0; e < 8; ++e) dw[k][e] = 0.f;
 
-  // Two passes per row: the row dot product, then dx and the dw partial
-  // (the second pass re-reads the row from L2; registers hold only dw).
-  for (int64_t row = row0 + wave; row < row_end; row += kRowsPerWg) {
+  // ONEPASS: the row's g and x stay in registers between the dot product
+  // and dx; otherwise (wide rows) the second pass re-reads them (L2).
+  for (int64_t row = row0 + wave; row < row_end; row += kBwdWaves) {
     const float r = RSTD[row];
     const lt_half* gp = dY + row * lddy;
     const lt_half* xp = X + row * ldx;
+    half8 gk[ONEPASS ? MAXK : 1], xk[ONEPASS ? MAXK : 1];
     float dot = 0.f;
 #pragma unroll
     for (int k = 0; k < MAXK; ++k) {
       const int c = lane + 64 * k;
+      half8 gv = as_half8(u32x4{0, 0, 0, 0}), xv = gv;
       if (c < nch) {
-        const half8 gv = as_half8(ld16(gp + c * 8));
-        const half8 xv = as_half8(ld16(xp + c * 8));
+        gv = as_half8(ld16(gp + c * 8));
+        xv = as_half8(ld16(xp + c * 8));
         const half8 wv = as_half8(ld16(W + c * 8));
 #pragma unroll
         for (int e = 0; e < 8; ++e) dot += (float)gv[e] * (float)wv[e] * (float)xv[e];
+      }
+      if constexpr (ONEPASS) {
+        gk[k] = gv;
+        xk[k] = xv;
       }
     }
     dot = wave_sum(dot);
@@ -118,8 +132,8 @@ rmsnorm_bwd_kernel(const lt_half* __restrict__ dY, int64_t lddy, const lt_half* 
     for (int k = 0; k < MAXK; ++k) {
       const int c = lane + 64 * k;
       if (c < nch) {
-        const half8 gv = as_half8(ld16(gp + c * 8));
-        const half8 xv = as_half8(ld16(xp + c * 8));
+        const half8 gv = ONEPASS ? gk[k] : as_half8(ld16(gp + c * 8));
+        const half8 xv = ONEPASS ? xk[k] : as_half8(ld16(xp + c * 8));
         const half8 wv = as_half8(ld16(W + c * 8));
         half8 rv = as_half8(u32x4{0, 0, 0, 0});
         if (R) rv = as_half8(ld16(R + row * ldr + c * 8));
@@ -135,15 +149,22 @@ rmsnorm_bwd_kernel(const lt_half* __restrict__ dY, int64_t lddy, const lt_half* 
     }
   }
 
-  float* dst = part + ((int64_t)blockIdx.x * kRowsPerWg + wave) * H;
+  // workgroup sum of the waves' partials, 512 columns at a time, in wave order
+  float* dst = part + (int64_t)blockIdx.x * H;
 #pragma unroll
   for (int k = 0; k < MAXK; ++k) {
-    const int c = lane + 64 * k;
-    if (c < nch) {
-      float4* d4 = reinterpret_cast<float4*>(dst + c * 8);
-      d4[0] = make_float4(dw[k][0], dw[k][1], dw[k][2], dw[k][3]);
-      d4[1] = make_float4(dw[k][4], dw[k][5], dw[k][6], dw[k][7]);
+    if (64 * k >= nch) break;                       // uniform
+#pragma unroll
+    for (int e = 0; e < 8; ++e) red[wave][lane * 8 + e] = dw[k][e];
+    __syncthreads();
+    const int t = threadIdx.x;                      // column 512 k + t
+    if (64 * k + t / 8 < nch) {
+      float sum = 0.f;
+#pragma unroll
+      for (int v = 0; v < kBwdWaves; ++v) sum += red[v][t];
+      dst[512 * k + t] = sum;
     }
+    __syncthreads();
   }
 }
 
@@ -232,17 +253,17 @@ hipError_t launch_rms_fwd(const lt_half* X, int64_t ldx, const lt_half* W, lt_ha
   return hipGetLastError();
 }
 
-template <int MAXK>
+template <int MAXK, bool ONEPASS>
 hipError_t launch_rms_bwd(const RmsBwdArgs& a, hipStream_t s) {
   const int nblk = rmsnorm_bwd_blocks(a.T);
   const int rows_per_wg = (int)((a.T + nblk - 1) / nblk);
-  hipLaunchKernelGGL((rmsnorm_bwd_kernel<MAXK>), dim3((unsigned)nblk), dim3(64 * kRowsPerWg), 0, s,
+  hipLaunchKernelGGL((rmsnorm_bwd_kernel<MAXK, ONEPASS>), dim3((unsigned)nblk), dim3(64 * kBwdWaves), 0, s,
                      a.dY, a.lddy, a.X, a.ldx, a.W, a.RSTD, a.R, a.ldr, a.dX, a.lddx, a.part, a.T,
                      (int)a.H, rows_per_wg);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(rmsnorm_dw_sum_kernel, dim3((unsigned)((a.H + 63) / 64)), dim3(64 * kSumWaves),
-                     0, s, a.part, nblk * kRowsPerWg, (int)a.H, a.dW);
+                     0, s, a.part, nblk, (int)a.H, a.dW);
   return hipGetLastError();
 }
 
@@ -260,9 +281,10 @@ hipError_t rmsnorm_fwd_launch(const lt_half* X, int64_t ldx, const lt_half* W, l
 
 hipError_t rmsnorm_bwd_launch(const RmsBwdArgs& a, hipStream_t s) {
   const int64_t k = (a.H / 8 + 63) / 64;
-  if (k <= 4) return launch_rms_bwd<4>(a, s);
-  if (k <= 8) return launch_rms_bwd<8>(a, s);
-  return launch_rms_bwd<16>(a, s);
+  if (k <= 4) return launch_rms_bwd<4, true>(a, s);
+  if (k <= 8) return launch_rms_bwd<8, true>(a, s);
+  if (k <= 12) return launch_rms_bwd<12, true>(a, s);
+  return launch_rms_bwd<16, false>(a, s);
 }
 
 hipError_t rope_table_launch(float* CS, int S, int D, double base, hipStream_t s) {
