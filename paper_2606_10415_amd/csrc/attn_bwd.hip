@@ -122,12 +122,12 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
   const int g = lane >> 5;
 
   const int bkv = blockIdx.x % (B * Hkv);
-  const int sp = (blockIdx.x / (B * Hkv)) % nsplit;   // which share of the query heads
+  const int sp = (blockIdx.x / (B * Hkv)) % nsplit;   // which share of the query blocks
   const int jt = blockIdx.x / (B * Hkv * nsplit);     // ascending key tile = descending work
   const int b = bkv / Hkv;
   const int kvh = bkv % Hkv;
-  const int grp = Hq / Hkv / nsplit;                  // query heads of this workgroup
-  const int h0 = kvh * (Hq / Hkv) + sp * grp;         // the first of them
+  const int G = Hq / Hkv;                             // query heads of the kv head
+  const int h0 = kvh * G;
   const int kbase = jt * BKV;
   const int kw0 = kbase + wave * 32;               // this wave's first key
   const int mykey = kw0 + lrow;                    // key owned by this lane (S, dP columns)
@@ -158,12 +158,18 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
   const int n_qb = (S + BQA - 1) / BQA;
   const int qb0 = causal ? kbase / BQA : 0;
   const int per_head = n_qb - qb0;
-  const int n_iter = grp * per_head;
+  // The group's (query head, query block) pairs, head-major, are split into
+  // nsplit contiguous shares; this workgroup takes share sp (possibly empty:
+  // its partial sums are then zero).
+  const int total = G * per_head;
+  const int it0 = (int)((int64_t)sp * total / nsplit);
+  const int n_iter = (int)((int64_t)(sp + 1) * total / nsplit) - it0;
 
-  // Block `it` = (query head, 32 queries).  Q, dO (rows past S read as zero)
+  // Block `it` = (query head, 64 queries).  Q, dO (rows past S read as zero)
   // and the base-2 LSE and D entries (zero past S: with zero Q and dO rows
   // those queries contribute nothing) go to LDS by direct loads.
-  auto block_of = [&](int it, int& h, int& qbase) {
+  auto block_of = [&](int i, int& h, int& qbase) {
+    const int it = it0 + i;
     h = h0 + it / per_head;
     qbase = (qb0 + it % per_head) * BQA;
   };

@@ -98,16 +98,29 @@ inline size_t attn_bwd_delta_bytes(int B, int S, int Hq) {
 }
 inline size_t attn_bwd_lse2_bytes(int B, int S, int Hq) { return attn_bwd_delta_bytes(B, S, Hq); }
 // The dK/dV pass runs one workgroup per (256-key tile, batch, kv head, split),
-// one workgroup per CU; with grouped queries and few kv heads the Hq/Hkv
-// query heads of a group are split over the smallest divisor n of Hq/Hkv that
-// gives at least 512 workgroups (all of them if none does), each writing FP32
-// partial sums.
+// one workgroup per CU.  A key tile's work is the (query head, 64-query block)
+// pairs of its group; when the tiles alone give fewer than 512 workgroups it
+// is split into n contiguous shares, each writing FP32 partial sums:
+//   * the smallest divisor n of Hq/Hkv that gives >= 512 workgroups (shares
+//     of whole query heads), if there is one;
+//   * otherwise n = min(max(Hq/Hkv, ceil(256 / tiles)), 16, the pairs of
+//     the last key tile, which has the fewest) -- e.g. a short causal MHA
+//     sequence.
+constexpr int64_t kDkdvFillWgs = 256;   // fallback split target: one workgroup per CU
 inline int attn_bwd_dkdv_splits(int B, int S, int Hq, int Hkv) {
   const int grp = Hq / Hkv;
-  const int64_t wgs = (int64_t)((S + 255) / 256) * B * Hkv;
-  for (int n = 1; n < grp; ++n)
+  const int n_kt = (S + 255) / 256;
+  const int64_t wgs = (int64_t)n_kt * B * Hkv;
+  if (wgs >= 512) return 1;
+  for (int n = 2; n <= grp; ++n)
     if (grp % n == 0 && wgs * n >= 512) return n;
-  return grp;
+  const int n_qb = (S + 63) / 64;
+  const int64_t last_pairs = (int64_t)grp * (n_qb - (n_kt - 1) * 4);   // causal: fewest pairs
+  int64_t n = (kDkdvFillWgs + wgs - 1) / wgs;
+  if (n < grp) n = grp;                                  // at least one share per query head
+  if (n > 16) n = 16;
+  if (n > last_pairs) n = last_pairs;
+  return n < 1 ? 1 : (int)n;
 }
 inline size_t attn_bwd_part_bytes(int B, int S, int Hq, int Hkv, int D) {
   const int n = attn_bwd_dkdv_splits(B, S, Hq, Hkv);
