@@ -103,15 +103,27 @@ def _align256(x):
 
 
 def test_attn_bwd_workspace():
-    # MHA: D and the base-2 LSE, [B, Hq, S] fp32 each, 256-byte aligned
-    assert lt.lt_attn_bwd_workspace_size(2, 100, 8, 8, 128) == 2 * _align256(4 * 2 * 8 * 100)
-    # GQA with few key tiles: plus fp32 partial dK, dV for every split of the group
-    # (here 4 splits of the 4 query heads per kv head)
+    # D and the base-2 LSE, [B, Hq, S] fp32 each, 256-byte aligned, plus fp32 partial
+    # dK, dV [2][n][B, S, Hkv, D] when a key tile's (query head, query block) pairs are
+    # split n ways (key tiles x B x Hkv < 512 workgroups): the smallest divisor of Hq/Hkv
+    # reaching 512 workgroups, else min(max(Hq/Hkv, ceil(256 / workgroups)), 16, the last
+    # key tile's pairs).
+    # MHA, S = 100: 16 workgroups, 2 query blocks in the only key tile -> n = 2
+    assert lt.lt_attn_bwd_workspace_size(2, 100, 8, 8, 128) == \
+        2 * _align256(4 * 2 * 8 * 100) + _align256(2 * 2 * 2 * 100 * 8 * 128 * 4)
+    # GQA 4:1, S = 100: 4 workgroups; max(4, 64) capped at 16, then at 4 heads x 2 blocks -> 8
     ws = lt.lt_attn_bwd_workspace_size(2, 100, 8, 2, 128)
-    assert ws == 2 * _align256(4 * 2 * 8 * 100) + _align256(2 * 4 * 2 * 100 * 2 * 128 * 4)
+    assert ws == 2 * _align256(4 * 2 * 8 * 100) + _align256(2 * 8 * 2 * 100 * 2 * 128 * 4)
     assert ws % 256 == 0
-    # enough kv heads x key tiles (1024 workgroups): no split, no partials
+    # MHA, S = 1024, 32 heads: 128 workgroups -> n = 2
+    assert lt.lt_attn_bwd_workspace_size(1, 1024, 32, 32, 128) == \
+        2 * _align256(4 * 32 * 1024) + _align256(2 * 2 * 1024 * 32 * 128 * 4)
+    # enough kv heads x key tiles (512 or more workgroups): no split, no partials
     assert lt.lt_attn_bwd_workspace_size(1, 4096, 128, 32, 128) == 2 * _align256(4 * 128 * 4096)
+    assert lt.lt_attn_bwd_workspace_size(1, 4096, 32, 32, 128) == 2 * _align256(4 * 32 * 4096)
+    # GQA 5:1 (Qwen2.5-32B heads), S = 4096: 128 workgroups, divisor 5 -> 640
+    assert lt.lt_attn_bwd_workspace_size(1, 4096, 40, 8, 128) == \
+        2 * _align256(4 * 40 * 4096) + _align256(2 * 5 * 4096 * 8 * 128 * 4)
     assert lt.lt_attn_bwd_workspace_size(0, 100, 8, 2, 128) == 0
     assert lt.lt_attn_bwd_workspace_size(1, 100, 8, 3, 128) == 0
     args = [FAKE, FAKE, FAKE, 1536, 1536, FAKE, FAKE, 1024, FAKE, FAKE, FAKE, FAKE, 1536, 1536]
