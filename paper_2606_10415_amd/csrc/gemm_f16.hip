@@ -32,7 +32,10 @@
 //   tiles (256x128 / 128x256) or, when the caller provides an FP32 workspace,
 //   as 256x256 tiles whose K is split over several workgroups (epilogue 3
 //   stores their partial sums; splitk_reduce_kernel adds them in a fixed
-//   order and applies alpha, beta * R and the bias).
+//   order and applies alpha, beta * R and the bias).  With a workspace, a
+//   launch of less than about one wave of 256x256 tiles is split the same
+//   way as a whole when the split gives twice the workgroups of 128x128 tiles
+//   or keeps a long K loop per split; else it runs as 128x128 tiles.
 #include <type_traits>
 
 #include "common.hpp"
@@ -644,7 +647,6 @@ hipError_t dispatch_tile(const GemmArgs& g, hipStream_t s) {
   const int64_t ncols = EPI == 1 ? g.F : g.N;
   const int64_t tm = (g.M + 255) / 256, tn = (ncols + unit_n - 1) / unit_n;
   const int64_t big_tiles = tm * tn;
-  if (big_tiles < 192) return launch<128, 128, 2, 2, 64, 2, TA, TB, EPI>(g, s);
   // A last wave at most half full runs as half-size tiles in one short round:
   // whole waves of 256x256 tiles first, then the remaining columns (or rows)
   // as 256x128 (or 128x256) tiles.
@@ -654,9 +656,10 @@ hipError_t dispatch_tile(const GemmArgs& g, hipStream_t s) {
   if constexpr (EPI == 0) {
     if (g.ws != nullptr && gemm_splitk_tail(g.M, g.N, g.K, &st) &&
         gemm_splitk_ws_bytes(g.M, g.N, g.K) <= g.ws_bytes) {
-      // The last wave as split-K 256x256 tiles: whole waves first (full K),
-      // then the remaining tiles' K split S ways (FP32 partials in the
-      // workspace), then the fixed-order sum with alpha, beta * R and bias.
+      // The last wave (or a launch of less than one wave) as split-K 256x256
+      // tiles: whole waves first (full K), then the remaining tiles' K split
+      // S ways (FP32 partials in the workspace), then the fixed-order sum
+      // with alpha, beta * R and bias.
       GemmArgs head = g, tail;
       if (st.columns) {
         head.N = st.split_at;
@@ -665,7 +668,8 @@ hipError_t dispatch_tile(const GemmArgs& g, hipStream_t s) {
         head.M = st.split_at;
         tail = row_part<TA, TB, 0>(g, st.split_at);
       }
-      hipError_t e = launch<256, 256, 2, 4, 64, 2, TA, TB, 0>(head, s);
+      hipError_t e = hipSuccess;
+      if (st.split_at > 0) e = launch<256, 256, 2, 4, 64, 2, TA, TB, 0>(head, s);
       if (e != hipSuccess) return e;
       GemmArgs part = tail;
       part.C = reinterpret_cast<lt_half*>(g.ws);
@@ -681,6 +685,7 @@ hipError_t dispatch_tile(const GemmArgs& g, hipStream_t s) {
       return hipGetLastError();
     }
   }
+  if (big_tiles < 192) return launch<128, 128, 2, 2, 64, 2, TA, TB, EPI>(g, s);
   if (waves >= 1 && rem > 0 && 2 * rem <= kCUs) {
     const int64_t full = waves * kCUs;
     if (full % tm == 0 && full / tm < tn) {
@@ -713,14 +718,31 @@ hipError_t dispatch_tile(const GemmArgs& g, hipStream_t s) {
 
 bool gemm_splitk_tail(int64_t M, int64_t N, int64_t K, SplitTail* p) {
   // the geometry of the half-tile tail (256x256 tiles, one wave = 256 CUs),
-  // with the last wave's K split so that its units fill about one wave
-  constexpr int64_t kCUs = 256, kMinSlices = 8, kMaxSplits = 8;
+  // with the last wave's K split so that its units fill about one wave; a
+  // launch of less than about one wave of 256x256 tiles is split whole
+  // (split_at = 0: no full-K part) when that beats 128x128 tiles with full
+  // K: the split gives twice their workgroups (S = 8) or each split still
+  // runs a long K loop (K / S >= kLongK); otherwise the workspace round trip
+  // costs more than the larger tile saves
+  constexpr int64_t kCUs = 256, kMinSlices = 8, kMaxSplits = 8, kLongK = 2048;
   if (M <= 0 || N <= 0 || K <= 0) return false;
   const int64_t tm = (M + 255) / 256, tn = (N + 255) / 256, tiles = tm * tn;
-  if (tiles < 192) return false;
+  const int64_t nk = (K + 63) / 64;
+  if (tiles < 192) {
+    int64_t S = kCUs / tiles;
+    if (S > kMaxSplits) S = kMaxSplits;
+    if (S > nk / kMinSlices) S = nk / kMinSlices;
+    if (S < 2) return false;
+    if (S < kMaxSplits && K < kLongK * S) return false;
+    p->columns = true;
+    p->split_at = 0;
+    p->Mt = M;
+    p->Nt = N;
+    p->S = (int)S;
+    return true;
+  }
   const int64_t waves = tiles / kCUs, rem = tiles % kCUs;
   if (waves < 1 || rem == 0 || 2 * rem > kCUs) return false;
-  const int64_t nk = (K + 63) / 64;
   int64_t S = kCUs / rem;
   if (S > kMaxSplits) S = kMaxSplits;
   if (S > nk / kMinSlices) S = nk / kMinSlices;

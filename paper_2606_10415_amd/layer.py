@@ -93,9 +93,11 @@ class DecoderLayer:
             self.dX = e(T, sh.H)
             self.ws_bytes = lt.lt_attn_bwd_workspace_size(sh.B, sh.S, sh.Hq, sh.Hkv, sh.D)
             self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.dev)
-            # split-K workspace of the plain GEMM calls (one at a time on the stream)
+            # split-K workspace of the plain GEMM calls (one at a time on the
+            # stream); the fused SwiGLU GEMMs take none
+            fused = ("gu_fwd", "down_dgrad") if self.fuse_swiglu else ()
             self.gemm_ws_bytes = max(lt.lt_gemm_f16_workspace_size(ta, tb, M, N, K)
-                                     for _, ta, tb, M, N, K in self._gemm_calls())
+                                     for n, ta, tb, M, N, K in self._gemm_calls() if n not in fused)
             self.gemm_ws = (torch.empty(self.gemm_ws_bytes, dtype=torch.uint8, device=self.dev)
                             if self.gemm_ws_bytes else None)
         self.dWqkv = e(*self.Wqkv.shape)

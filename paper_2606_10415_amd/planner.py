@@ -104,12 +104,14 @@ class ModelProfile:
         return 2 * b * S * self.H
 
     def gemm_workspace(self, b, S):
-        """FP32 split-K workspace of the layer's GEMMs (the largest any of its 12
-        GEMM shapes asks the library for; one at a time on the stream)."""
+        """FP32 split-K workspace of the layer's GEMMs (the largest any of its 10
+        plain GEMM shapes asks the library for; one at a time on the stream; the
+        gate/up forward and the down-projection input gradient run with the
+        fused SwiGLU epilogues, which take none)."""
         from . import lt
         T, Hd = b * S, self.Hq * self.D
-        shapes = [(T, self.qkv_cols, self.H), (T, self.H, Hd), (T, 2 * self.F, self.H),
-                  (T, self.H, self.F), (self.H, self.F, T), (T, self.F, self.H),
+        shapes = [(T, self.qkv_cols, self.H), (T, self.H, Hd),
+                  (T, self.H, self.F), (self.H, self.F, T),
                   (2 * self.F, self.H, T), (T, self.H, 2 * self.F), (self.H, Hd, T),
                   (T, Hd, self.H), (self.qkv_cols, self.H, T), (T, self.H, self.qkv_cols)]
         return max(lt.lt_gemm_f16_workspace_size(0, 0, M, N, K) for M, N, K in shapes)

@@ -306,7 +306,9 @@ def test_bias_grad_workspace_and_empty():
 
 # Split-K workspace of the last, at most half full, wave of 256x256 tiles (256 CUs):
 # S = min(256 // tail_tiles, 8, ceil(K/64) // 8) splits (none below 2), FP32 partials
-# over the tail region: S * Mt * Nt * 4 bytes.
+# over the tail region: S * Mt * Nt * 4 bytes.  A launch of fewer than 192 tiles is
+# split whole, S = min(256 // tiles, 8, ceil(K/64) // 8) over all of M x N, when
+# S = 8 or K >= 2048 * S.
 @pytest.mark.parametrize("M,N,K,want", [
     (4096, 5120, 5120, 4 * 4096 * 1024 * 4),    # 16x20 tiles: 64 in the tail, columns 4096..5119
     (5120, 4096, 4096, 4 * 1024 * 4096 * 4),    # 20x16 tiles: rows 4096..5119
@@ -316,7 +318,13 @@ def test_bias_grad_workspace_and_empty():
     (4096, 5120, 512, 0),                       # 8 K-slices: too few to split
     (4096, 4096, 4096, 0),                      # whole waves only
     (4096, 7168, 5120, 0),                      # 448 tiles: last wave 3/4 full
-    (1024, 1024, 8192, 0),                      # 16 tiles: 128x128 tiles, no tail
+    (1024, 1024, 8192, 8 * 1024 * 1024 * 4),    # 16 tiles, split whole: S = 8
+    (2048, 4096, 4096, 2 * 2048 * 4096 * 4),    # 128 tiles, split whole: S = 2
+    (2048, 4096, 1000, 0),                      # S = 2 but K < 4096: 128x128 tiles
+    (2048, 2048, 2048, 0),                      # 64 tiles, S = 4, K < 8192
+    (1024, 1024, 4096, 8 * 1024 * 1024 * 4),    # S = 8 at any K
+    (2048, 3000, 4104, 2 * 2048 * 3000 * 4),    # 96 tiles, S = 2, ragged K >= 4096
+    (256, 256, 256, 0),                         # 4 K-slices: too few to split
     (0, 5120, 5120, 0), (4096, 5120, 0, 0),
 ])
 def test_gemm_workspace_size(M, N, K, want):

@@ -170,6 +170,9 @@ def _tail_rows(M, n=40, seed=3):
     (4096, 5120, 2048, False, False),   # column tail (columns 4096..), S = 4
     (5120, 4096, 1024, True, False),    # row tail (rows 4096..), S = 2, bias
     (4088, 5112, 1000, False, True),    # ragged M/N/K, ragged last split, C = R in place
+    (1024, 1536, 4096, True, False),    # 24 tiles, split whole (S = 8), bias
+    (1000, 1544, 4136, False, True),    # 28 tiles, split whole (S = 8), ragged, in place
+    (2048, 3000, 4104, False, False),   # 96 tiles, split whole (S = 2), ragged N and K
 ])
 def test_gemm_ws_split_tail_exact_integers(env, transA, transB, M, N, K, bias, inplace):
     """Integer-valued inputs keep every FP32 partial and sum exact, so the split
