@@ -45,9 +45,9 @@ GEMM_TRAFFIC = {
     "workload": "llama2-7b",
     "layer": "paper",
     "fuse_swiglu": True,
-    "sources_sha256": "2ef160f073b004ca13455e5ef51f98d96eba678db8c067e897fd91c9d82a4ea8",
-    "fetch_bytes_per_launch": 664574840,
-    "write_bytes_per_launch": 100061412,
+    "sources_sha256": "c4d454f978e0802ef87dd5dcb1d6886726658401e62d0402a4a84ec4f793d469",
+    "fetch_bytes_per_launch": 664126981,
+    "write_bytes_per_launch": 99934228,
 }
 GEMM_SOURCES = ("paper_2606_10415_amd/csrc/gemm_f16.hip", "paper_2606_10415_amd/csrc/common.hpp")
 
