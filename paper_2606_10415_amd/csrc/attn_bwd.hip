@@ -33,6 +33,13 @@
 //                     loads, double-buffered), recomputing S^T and dP^T with
 //                     one query per lane; dQ^T += K^T dS^T reads K^T through the
 //                     transpose read.  dQ is written once, in FP16.
+//                     Short sequences (under 512 such workgroups) take
+//                     128-query workgroups instead: waves w and w + 4 own the
+//                     same 32 queries and take alternate 32-key blocks, and
+//                     their FP32 accumulators are added through LDS at the
+//                     end, which doubles the workgroups and halves the
+//                     longest causal tile.  Key blocks wholly above a wave's
+//                     queries are skipped.
 // Kernels 2 and 3 both recompute S and dP: seven contractions instead of
 // five, traded for no dQ atomics (whose traffic would exceed the whole
 // algorithmic byte count several times) and two waves per SIMD in each.
@@ -50,6 +57,7 @@ constexpr int BQA = 64;        // dK/dV: queries per block (two 32-query halves)
 constexpr int NW = 8;          // dQ: waves per workgroup
 constexpr int BQB = NW * 32;   // dQ: queries per workgroup (32 per wave)
 constexpr int BKB = 128;       // dQ: keys per slice
+constexpr int64_t kDqFillWgs = 512;   // dQ: 256-query workgroups needed to skip the split
 constexpr float kLog2e = 1.4426950408889634f;
 
 // ------------------------------------------------------------ kernel 1
@@ -347,7 +355,12 @@ struct DqSmem {
   static constexpr int STAGE = 2 * TILE;          // K then V
 };
 
-template <int D>
+// QSPLIT = 1: 8 query groups of 32 (256 queries), every wave walks every
+// 32-key block.  QSPLIT = 2 (short sequences, for twice the workgroups): 4
+// query groups (128 queries); waves w and w + 4 share a query group and take
+// alternate 32-key blocks of each slice, and their FP32 accumulators are
+// summed through LDS at the end (wave w + 4's into wave w's, fixed order).
+template <int D, int QSPLIT>
 __global__ void __launch_bounds__(NW * 64, 2)
 attn_bwd_dq_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
                    const lt_half* __restrict__ V, int64_t q_stride, int64_t kv_stride,
@@ -359,6 +372,10 @@ attn_bwd_dq_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
   constexpr int KB = BKB / 32;     // 32-key blocks per slice
   constexpr int DB = D / 32;
   constexpr int KK = D / 16;
+  constexpr int NQG = NW / QSPLIT;                 // query groups of 32
+  constexpr int BQ = NQG * 32;                     // queries per workgroup
+  static_assert(NW % QSPLIT == 0 && KB % QSPLIT == 0, "QSPLIT must divide waves and blocks");
+  static_assert(QSPLIT == 1 || NQG * DB * 4 * 64 * 16 <= 2 * SM::STAGE, "reduction fits in LDS");
   __shared__ __attribute__((aligned(1024))) char smem[2 * SM::STAGE];
 
   const int tid = threadIdx.x;
@@ -366,15 +383,17 @@ attn_bwd_dq_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar addressing
   const int lrow = lane & 31;
   const int g = lane >> 5;
+  const int qg = wave % NQG;                       // query group
+  const int kpart = wave / NQG;                    // which of the QSPLIT key-block shares
 
-  const int n_qt = (S + BQB - 1) / BQB;
+  const int n_qt = (S + BQ - 1) / BQ;
   const int bh = blockIdx.x % (B * Hq);
   const int qt = causal ? n_qt - 1 - (int)(blockIdx.x / (B * Hq)) : (int)(blockIdx.x / (B * Hq));
   const int b = bh / Hq;
   const int h = bh % Hq;
   const int kvh = h / (Hq / Hkv);
-  const int q0 = qt * BQB;
-  const int qw0 = q0 + wave * 32;
+  const int q0 = qt * BQ;
+  const int qw0 = q0 + qg * 32;
   const int myq = qw0 + lrow;                      // query owned by this lane
 
   const lt_half* Kp = K + (int64_t)b * S * kv_stride + (int64_t)kvh * D;
@@ -411,7 +430,7 @@ attn_bwd_dq_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
 #pragma unroll
     for (int r = 0; r < 16; ++r) dqacc[db][r] = 0.f;
 
-  const int kv_end = causal ? min(S, q0 + BQB) : S;
+  const int kv_end = causal ? min(S, q0 + BQ) : S;
   const int n_kv = (kv_end + BKB - 1) / BKB;
   const int q_hi = min(qw0 + 32, S) - 1;           // last valid query of this wave
   const int klim = causal ? min(myq + 1, S) : S;   // keys < klim are visible
@@ -447,6 +466,8 @@ attn_bwd_dq_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
       const bool need_mask = (causal && key0 + BKB - 1 > qw0) || key0 + BKB > S;   // wave-uniform
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
+        if (QSPLIT > 1 && kb % QSPLIT != kpart) continue;
+        if (causal && key0 + kb * 32 > q_hi) continue;   // block above every query of the wave
         //   S^T = K Q^T, dP^T = V dO^T   (lane owns query `myq`, 16 key rows)
         f32x16 sacc, pacc;
 #pragma unroll
@@ -488,6 +509,39 @@ attn_bwd_dq_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
     // next slice resident for every wave; nobody reads this stage any more
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+  }
+
+  if constexpr (QSPLIT > 1) {
+    // every stage is free after the loop's last barrier; the partner waves'
+    // accumulators go through LDS in the accumulator layout (lane-major
+    // float4, conflict-free) and are added in share order
+    float4* red = reinterpret_cast<float4*>(smem);
+    for (int part = QSPLIT - 1; part >= 1; --part) {
+      if (kpart == part) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int rq = 0; rq < 4; ++rq)
+            red[((qg * DB + db) * 4 + rq) * 64 + lane] =
+                make_float4(dqacc[db][4 * rq], dqacc[db][4 * rq + 1], dqacc[db][4 * rq + 2],
+                            dqacc[db][4 * rq + 3]);
+      }
+      __syncthreads();
+      if (kpart == part - 1) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int rq = 0; rq < 4; ++rq) {
+            const float4 v = red[((qg * DB + db) * 4 + rq) * 64 + lane];
+            dqacc[db][4 * rq] += v.x;
+            dqacc[db][4 * rq + 1] += v.y;
+            dqacc[db][4 * rq + 2] += v.z;
+            dqacc[db][4 * rq + 3] += v.w;
+          }
+      }
+      __syncthreads();
+    }
+    if (kpart != 0) return;
   }
 
   // ---- dQ = scale * acc -> FP16 ----
@@ -566,11 +620,21 @@ hipError_t launch_bwd(const AttnBwdArgs& a, hipStream_t s) {
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  const int n_qt = (sh.S + BQB - 1) / BQB;
-  hipLaunchKernelGGL((attn_bwd_dq_kernel<D>), dim3((unsigned)(n_qt * sh.B * sh.Hq)),
-                     dim3(NW * 64), 0, s, a.Q, a.K, a.V, a.q_stride, a.kv_stride, a.dO, a.o_stride,
-                     a.lse2, a.delta, a.dQ, a.dq_stride, sh.B, sh.S, sh.Hq, sh.Hkv, sh.scale,
-                     sh.causal);
+  // 256-query workgroups while they give at least two per CU, else 128
+  const int64_t wgs256 = (int64_t)((sh.S + BQB - 1) / BQB) * sh.B * sh.Hq;
+  if (wgs256 >= kDqFillWgs) {
+    const int n_qt = (sh.S + BQB - 1) / BQB;
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<D, 1>), dim3((unsigned)(n_qt * sh.B * sh.Hq)),
+                       dim3(NW * 64), 0, s, a.Q, a.K, a.V, a.q_stride, a.kv_stride, a.dO,
+                       a.o_stride, a.lse2, a.delta, a.dQ, a.dq_stride, sh.B, sh.S, sh.Hq, sh.Hkv,
+                       sh.scale, sh.causal);
+  } else {
+    const int n_qt = (sh.S + BQB / 2 - 1) / (BQB / 2);
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<D, 2>), dim3((unsigned)(n_qt * sh.B * sh.Hq)),
+                       dim3(NW * 64), 0, s, a.Q, a.K, a.V, a.q_stride, a.kv_stride, a.dO,
+                       a.o_stride, a.lse2, a.delta, a.dQ, a.dq_stride, sh.B, sh.S, sh.Hq, sh.Hkv,
+                       sh.scale, sh.causal);
+  }
   return hipGetLastError();
 }
 

@@ -131,6 +131,11 @@ CASES = [
     (1, 384, 8, 2, 128, True),     # several tiles of every kernel
     (1, 130, 4, 4, 64, False),     # non-causal, ragged
     (2, 256, 4, 1, 128, False),    # non-causal, MQA
+    # dQ: under 512 workgroups of 256 queries the launch takes 128-query
+    # workgroups whose wave pairs split the key blocks (every case above);
+    # these two have 512 and keep 256-query workgroups
+    (2, 300, 128, 16, 64, True),   # ragged, GQA 8:1
+    (1, 264, 256, 64, 64, False),  # non-causal, ragged
 ]
 
 
