@@ -201,12 +201,15 @@ lt_status lt_attn_fwd(const lt_half* Q, const lt_half* K, const lt_half* V,
 /*
  * Bytes of device workspace lt_attn_bwd needs: the per-row term
  * D_i = rowsum(dO_i * O_i) [B, Hq, S] FP32 and the row LSE in base 2
- * [B, Hq, S] FP32, each 256-byte aligned; when the 256-key tiles of all
- * batches and key/value heads give fewer than 512 workgroups (few kv heads,
- * short sequences) also FP32 partial dK and dV sums [2][n][B, S, Hkv, D]:
- * each key tile's (query head, 64-query block) pairs are then split into n
- * contiguous shares, one workgroup each, and the partials are summed in a
- * fixed order, so results stay deterministic.  0 for invalid sizes.
+ * [B, Hq, S] FP32, each 256-byte aligned.  The dK/dV pass takes 256-key
+ * tiles, except for MHA (Hq = Hkv) when those give fewer than 512
+ * workgroups over all batches and key/value heads: then 128-key tiles.
+ * When the chosen tiles still give
+ * fewer than 512 workgroups (few kv heads, short sequences) the workspace
+ * also holds FP32 partial dK and dV sums [2][n][B, S, Hkv, D]: each key
+ * tile's (query head, 64-query block) pairs are then split into n contiguous
+ * shares, one workgroup each, and the partials are summed in a fixed order,
+ * so results stay deterministic.  0 for invalid sizes.
  */
 size_t lt_attn_bwd_workspace_size(int B, int S, int Hq, int Hkv, int D);
 

@@ -22,10 +22,15 @@
 //                     dS feed the dV / dK MFMAs from registers; their Q^T /
 //                     dO^T operands come from the same row-layout tiles through
 //                     the LDS transpose read, in the accumulators' query order.
-//                     With grouped queries and few kv heads the group's query
-//                     heads are split over several workgroups, whose FP32
-//                     partial dK, dV go to the workspace and are summed in a
-//                     fixed order by attn_bwd_dkdv_sum (kernel 4).
+//                     When 256-key tiles give too few workgroups (short
+//                     sequences, few kv heads) the tiles hold 128 keys: waves
+//                     w and w + 4 own the same keys, take the two 32-query
+//                     halves of each block, and add their accumulators
+//                     through LDS at the end.  Still too few: each key tile's
+//                     (query head, query block) work is split over several
+//                     workgroups, whose FP32 partial dK, dV go to the
+//                     workspace and are summed in a fixed order by
+//                     attn_bwd_dkdv_sum (kernel 4).
 //   3. attn_bwd_dq  : query-major, the forward's layout.  One workgroup per
 //                     (batch, head, 256-query tile, 8 waves); each wave owns 32 queries
 //                     (Q and dO fragments and the dQ accumulator in registers)
@@ -109,7 +114,11 @@ struct DkdvSmem {
   static constexpr int BYTES = ROW_OFF + 4 * 256;
 };
 
-template <int D>
+// KSPLIT = 1: 8 key groups of 32 (256 keys), every wave walks both 32-query
+// halves of each block.  KSPLIT = 2 (few workgroups): 4 key groups (128
+// keys); waves w and w + 4 own the same keys, take one half each, and their
+// FP32 accumulators are summed through LDS at the end (fixed order).
+template <int D, int KSPLIT>
 __global__ void __launch_bounds__(NWA * 64, 1)
 attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
                      const lt_half* __restrict__ V, int64_t q_stride, int64_t kv_stride,
@@ -121,6 +130,10 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
   using RT = RowTile<D, NWA>;
   constexpr int KK = D / 16;       // MFMA steps over the head dim
   constexpr int DB = D / 32;       // 32-feature blocks
+  constexpr int NKG = NWA / KSPLIT;                // key groups of 32
+  constexpr int BK = NKG * 32;                     // keys per workgroup
+  static_assert(KSPLIT == 1 || KSPLIT == BQA / 32, "one 32-query half per wave of a pair");
+  static_assert(KSPLIT == 1 || NKG * 2 * DB * 4 * 64 * 16 <= SM::BYTES, "reduction fits in LDS");
   __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
 
   const int tid = threadIdx.x;
@@ -128,6 +141,8 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar addressing
   const int lrow = lane & 31;
   const int g = lane >> 5;
+  const int kg = wave % NKG;                       // key group
+  const int kpart = wave / NKG;                    // query half taken (KSPLIT = 2)
 
   const int bkv = blockIdx.x % (B * Hkv);
   const int sp = (blockIdx.x / (B * Hkv)) % nsplit;   // which share of the query blocks
@@ -136,16 +151,16 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
   const int kvh = bkv % Hkv;
   const int G = Hq / Hkv;                             // query heads of the kv head
   const int h0 = kvh * G;
-  const int kbase = jt * BKV;
-  const int kw0 = kbase + wave * 32;               // this wave's first key
+  const int kbase = jt * BK;
+  const int kw0 = kbase + kg * 32;                 // this wave's first key
   const int mykey = kw0 + lrow;                    // key owned by this lane (S, dP columns)
 
   const lt_half* Kp = K + (int64_t)b * S * kv_stride + (int64_t)kvh * D;
   const lt_half* Vp = V + (int64_t)b * S * kv_stride + (int64_t)kvh * D;
 
   // ---- V tile -> LDS (B operand of dP = dO V^T); rows past S read as zero ----
-  RT::template dma<BKV>(smem + SM::V_OFF, Vp + (int64_t)kbase * kv_stride, kv_stride, S - kbase,
-                        wave, lane);
+  RT::template dma<BK>(smem + SM::V_OFF, Vp + (int64_t)kbase * kv_stride, kv_stride, S - kbase,
+                       wave, lane);
   // ---- K fragments (B operand of S = Q K^T) ----
   half8 kf[KK];
 #pragma unroll
@@ -216,7 +231,8 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
     const float* del_s = reinterpret_cast<const float*>(smem + SM::ROW_OFF + cur * 512 + 256);
 
 #pragma nounroll
-    for (int hq = 0; hq < BQA / 32; ++hq) {
+    for (int ih = 0; ih < BQA / 32 / KSPLIT; ++ih) {
+    const int hq = KSPLIT > 1 ? kpart : ih;
     // 32-query half hq of the block; causal: all of this wave's keys after
     // all of its queries -> P = 0
     const int qh = qbase + hq * 32;
@@ -234,7 +250,7 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
       // fragments of step kk+1 are read before the MFMAs of step kk
       half8 fq = RT::row_frag(qs, hq * 32, 0, lane);
       half8 fd = RT::row_frag(dos, hq * 32, 0, lane);
-      half8 fv = RT::row_frag(smem + SM::V_OFF, wave * 32, 0, lane);
+      half8 fv = RT::row_frag(smem + SM::V_OFF, kg * 32, 0, lane);
       __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
@@ -242,7 +258,7 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
         if (kk + 1 < KK) {
           nq = RT::row_frag(qs, hq * 32, kk + 1, lane);
           nd = RT::row_frag(dos, hq * 32, kk + 1, lane);
-          nv = RT::row_frag(smem + SM::V_OFF, wave * 32, kk + 1, lane);
+          nv = RT::row_frag(smem + SM::V_OFF, kg * 32, kk + 1, lane);
         }
         sacc = mfma32(fq, kf[kk], sacc);
         pacc = mfma32(fd, fv, pacc);
@@ -307,6 +323,44 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
     // next block resident for every wave; nobody reads this buffer any more
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+  }
+
+  if constexpr (KSPLIT > 1) {
+    // all of LDS is free after the loop's last barrier: the second wave of
+    // each pair passes its dK, dV accumulators through it (lane-major float4,
+    // conflict-free) to the first, which adds them
+    float4* red = reinterpret_cast<float4*>(smem);
+    auto slot = [&](int which, int db, int rq) { return ((kg * 2 + which) * DB + db) * 4 + rq; };
+    if (kpart == 1) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int rq = 0; rq < 4; ++rq) {
+          red[slot(0, db, rq) * 64 + lane] =
+              make_float4(dkacc[db][4 * rq], dkacc[db][4 * rq + 1], dkacc[db][4 * rq + 2],
+                          dkacc[db][4 * rq + 3]);
+          red[slot(1, db, rq) * 64 + lane] =
+              make_float4(dvacc[db][4 * rq], dvacc[db][4 * rq + 1], dvacc[db][4 * rq + 2],
+                          dvacc[db][4 * rq + 3]);
+        }
+    }
+    __syncthreads();
+    if (kpart != 0) return;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        const float4 k = red[slot(0, db, rq) * 64 + lane];
+        const float4 v = red[slot(1, db, rq) * 64 + lane];
+        dkacc[db][4 * rq] += k.x;
+        dkacc[db][4 * rq + 1] += k.y;
+        dkacc[db][4 * rq + 2] += k.z;
+        dkacc[db][4 * rq + 3] += k.w;
+        dvacc[db][4 * rq] += v.x;
+        dvacc[db][4 * rq + 1] += v.y;
+        dvacc[db][4 * rq + 2] += v.z;
+        dvacc[db][4 * rq + 3] += v.w;
+      }
   }
 
   // ---- write dK = scale * acc, dV (or this split's FP32 partial sums) ----
@@ -604,12 +658,20 @@ hipError_t launch_bwd(const AttnBwdArgs& a, hipStream_t s) {
                      a.o_stride, a.LSE, a.delta, a.lse2, sh.B, sh.S, sh.Hq);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int n_kt = (sh.S + BKV - 1) / BKV;
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D>),
-                     dim3((unsigned)(n_kt * sh.B * sh.Hkv * a.nsplit)), dim3(NWA * 64), 0, s, a.Q,
-                     a.K, a.V, a.q_stride, a.kv_stride, a.dO, a.o_stride, a.lse2, a.delta, a.dK,
-                     a.dV, a.dkv_stride, a.part, a.nsplit, sh.B, sh.S, sh.Hq, sh.Hkv, sh.scale,
-                     sh.causal);
+  const int n_kt = (sh.S + a.ktile - 1) / a.ktile;
+  const dim3 kgrid((unsigned)(n_kt * sh.B * sh.Hkv * a.nsplit));
+  if (a.ktile == BKV)
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, 1>), kgrid, dim3(NWA * 64), 0, s, a.Q, a.K, a.V,
+                       a.q_stride, a.kv_stride, a.dO, a.o_stride, a.lse2, a.delta, a.dK, a.dV,
+                       a.dkv_stride, a.part, a.nsplit, sh.B, sh.S, sh.Hq, sh.Hkv, sh.scale,
+                       sh.causal);
+  else if (a.ktile == BKV / 2)
+    hipLaunchKernelGGL((attn_bwd_dkdv_kernel<D, 2>), kgrid, dim3(NWA * 64), 0, s, a.Q, a.K, a.V,
+                       a.q_stride, a.kv_stride, a.dO, a.o_stride, a.lse2, a.delta, a.dK, a.dV,
+                       a.dkv_stride, a.part, a.nsplit, sh.B, sh.S, sh.Hq, sh.Hkv, sh.scale,
+                       sh.causal);
+  else
+    return hipErrorInvalidValue;
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (a.nsplit > 1) {

@@ -88,7 +88,8 @@ struct AttnBwdArgs {
   float* delta;   // workspace: [B, Hq, S]  rowsum(dO * O)
   float* lse2;    // workspace: [B, Hq, S]  LSE * log2(e)
   float* part;    // workspace: [2][nsplit][B, S, Hkv, D] partial dK, dV (nsplit > 1 only)
-  int nsplit;     // query-head groups per key tile of the dK/dV pass
+  int nsplit;     // shares of each key tile's work in the dK/dV pass
+  int ktile;      // keys per dK/dV workgroup (256 or 128)
 };
 
 // Workspace layout of the attention backward (offsets in bytes).
@@ -97,33 +98,43 @@ inline size_t attn_bwd_delta_bytes(int B, int S, int Hq) {
   return align256((size_t)B * Hq * S * sizeof(float));
 }
 inline size_t attn_bwd_lse2_bytes(int B, int S, int Hq) { return attn_bwd_delta_bytes(B, S, Hq); }
-// The dK/dV pass runs one workgroup per (256-key tile, batch, kv head, split),
-// one workgroup per CU.  A key tile's work is the (query head, 64-query block)
-// pairs of its group; when the tiles alone give fewer than 512 workgroups it
-// is split into n contiguous shares, each writing FP32 partial sums:
+// The dK/dV pass runs one workgroup per (key tile, batch, kv head, share),
+// one workgroup per CU.  Key tiles hold 256 keys (8 waves of 32), except
+// for MHA (Hq = Hkv) when those give fewer than 512 workgroups: then 128
+// keys, waves w and w + 4 owning the same 32 keys and taking the two
+// 32-query halves of every 64-query block.  (With grouped queries the 256-key
+// tile's shares of whole query heads measured faster.)
+// A key tile's work is the (query head, 64-query block) pairs of its group;
+// when the tiles alone give fewer than 512 workgroups it is split into n
+// contiguous shares, each writing FP32 partial sums:
 //   * the smallest divisor n of Hq/Hkv that gives >= 512 workgroups (shares
 //     of whole query heads), if there is one;
 //   * otherwise n = min(max(Hq/Hkv, ceil(256 / tiles)), 16, the pairs of
 //     the last key tile, which has the fewest) -- e.g. a short causal MHA
 //     sequence.
 constexpr int64_t kDkdvFillWgs = 256;   // fallback split target: one workgroup per CU
-inline int attn_bwd_dkdv_splits(int B, int S, int Hq, int Hkv) {
+struct DkdvPlan {
+  int ktile;    // keys per workgroup: 256 or 128
+  int nsplit;   // shares of each key tile's work
+};
+inline DkdvPlan attn_bwd_dkdv_plan(int B, int S, int Hq, int Hkv) {
   const int grp = Hq / Hkv;
-  const int n_kt = (S + 255) / 256;
+  const int ktile = grp > 1 || (int64_t)((S + 255) / 256) * B * Hkv >= 512 ? 256 : 128;
+  const int n_kt = (S + ktile - 1) / ktile;
   const int64_t wgs = (int64_t)n_kt * B * Hkv;
-  if (wgs >= 512) return 1;
+  if (wgs >= 512) return {ktile, 1};
   for (int n = 2; n <= grp; ++n)
-    if (grp % n == 0 && wgs * n >= 512) return n;
+    if (grp % n == 0 && wgs * n >= 512) return {ktile, n};
   const int n_qb = (S + 63) / 64;
-  const int64_t last_pairs = (int64_t)grp * (n_qb - (n_kt - 1) * 4);   // causal: fewest pairs
+  const int64_t last_pairs = (int64_t)grp * (n_qb - (int64_t)(n_kt - 1) * (ktile / 64));
   int64_t n = (kDkdvFillWgs + wgs - 1) / wgs;
   if (n < grp) n = grp;                                  // at least one share per query head
   if (n > 16) n = 16;
   if (n > last_pairs) n = last_pairs;
-  return n < 1 ? 1 : (int)n;
+  return {ktile, n < 1 ? 1 : (int)n};
 }
 inline size_t attn_bwd_part_bytes(int B, int S, int Hq, int Hkv, int D) {
-  const int n = attn_bwd_dkdv_splits(B, S, Hq, Hkv);
+  const int n = attn_bwd_dkdv_plan(B, S, Hq, Hkv).nsplit;
   return n > 1 ? align256((size_t)2 * n * B * S * Hkv * D * sizeof(float)) : 0;
 }
 

@@ -239,7 +239,10 @@ lt_status lt_attn_bwd(const lt_half* Q, const lt_half* K, const lt_half* V, int6
                     reinterpret_cast<float*>(ws + lt::attn_bwd_delta_bytes(B, S, Hq)),
                     reinterpret_cast<float*>(ws + lt::attn_bwd_delta_bytes(B, S, Hq) +
                                              lt::attn_bwd_lse2_bytes(B, S, Hq)),
-                    lt::attn_bwd_dkdv_splits(B, S, Hq, Hkv)};
+                    0, 0};
+  const lt::DkdvPlan plan = lt::attn_bwd_dkdv_plan(B, S, Hq, Hkv);
+  a.nsplit = plan.nsplit;
+  a.ktile = plan.ktile;
   return from_hip(lt::attn_bwd_launch(a, reinterpret_cast<hipStream_t>(stream)), "attn_bwd launch");
 }
 

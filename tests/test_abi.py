@@ -105,9 +105,11 @@ def _align256(x):
 def test_attn_bwd_workspace():
     # D and the base-2 LSE, [B, Hq, S] fp32 each, 256-byte aligned, plus fp32 partial
     # dK, dV [2][n][B, S, Hkv, D] when a key tile's (query head, query block) pairs are
-    # split n ways (key tiles x B x Hkv < 512 workgroups): the smallest divisor of Hq/Hkv
-    # reaching 512 workgroups, else min(max(Hq/Hkv, ceil(256 / workgroups)), 16, the last
-    # key tile's pairs).
+    # split n ways.  Key tiles hold 256 keys, or 128 for MHA when 256-key tiles give fewer
+    # than 512 workgroups (tiles x B x Hkv); with the chosen tiles, fewer than 512
+    # workgroups split n ways: the
+    # smallest divisor of Hq/Hkv reaching 512 workgroups, else min(max(Hq/Hkv,
+    # ceil(256 / workgroups)), 16, the last key tile's pairs).
     # MHA, S = 100: 16 workgroups, 2 query blocks in the only key tile -> n = 2
     assert lt.lt_attn_bwd_workspace_size(2, 100, 8, 8, 128) == \
         2 * _align256(4 * 2 * 8 * 100) + _align256(2 * 2 * 2 * 100 * 8 * 128 * 4)
@@ -115,13 +117,18 @@ def test_attn_bwd_workspace():
     ws = lt.lt_attn_bwd_workspace_size(2, 100, 8, 2, 128)
     assert ws == 2 * _align256(4 * 2 * 8 * 100) + _align256(2 * 8 * 2 * 100 * 2 * 128 * 4)
     assert ws % 256 == 0
-    # MHA, S = 1024, 32 heads: 128 workgroups -> n = 2
-    assert lt.lt_attn_bwd_workspace_size(1, 1024, 32, 32, 128) == \
-        2 * _align256(4 * 32 * 1024) + _align256(2 * 2 * 1024 * 32 * 128 * 4)
+    # MHA, S = 1024, 32 heads: 128-key tiles, 256 workgroups -> n = 1, no partials
+    assert lt.lt_attn_bwd_workspace_size(1, 1024, 32, 32, 128) == 2 * _align256(4 * 32 * 1024)
+    # MHA, S = 512: 128 workgroups of 128 keys; the last tile has 2 query blocks -> n = 2
+    assert lt.lt_attn_bwd_workspace_size(1, 512, 32, 32, 128) == \
+        2 * _align256(4 * 32 * 512) + _align256(2 * 2 * 512 * 32 * 128 * 4)
+    # GQA 5:1, S = 2048: 64 workgroups of 256 keys, no divisor reaches 512 -> max(4, 5)
+    assert lt.lt_attn_bwd_workspace_size(1, 2048, 40, 8, 128) == \
+        2 * _align256(4 * 40 * 2048) + _align256(2 * 5 * 2048 * 8 * 128 * 4)
     # enough kv heads x key tiles (512 or more workgroups): no split, no partials
     assert lt.lt_attn_bwd_workspace_size(1, 4096, 128, 32, 128) == 2 * _align256(4 * 128 * 4096)
     assert lt.lt_attn_bwd_workspace_size(1, 4096, 32, 32, 128) == 2 * _align256(4 * 32 * 4096)
-    # GQA 5:1 (Qwen2.5-32B heads), S = 4096: 128 workgroups, divisor 5 -> 640
+    # GQA 5:1 (Qwen2.5-32B heads), S = 4096: 128 workgroups of 256 keys, divisor 5 -> 640
     assert lt.lt_attn_bwd_workspace_size(1, 4096, 40, 8, 128) == \
         2 * _align256(4 * 40 * 4096) + _align256(2 * 5 * 4096 * 8 * 128 * 4)
     assert lt.lt_attn_bwd_workspace_size(0, 100, 8, 2, 128) == 0

@@ -131,11 +131,14 @@ CASES = [
     (1, 384, 8, 2, 128, True),     # several tiles of every kernel
     (1, 130, 4, 4, 64, False),     # non-causal, ragged
     (2, 256, 4, 1, 128, False),    # non-causal, MQA
-    # dQ: under 512 workgroups of 256 queries the launch takes 128-query
-    # workgroups whose wave pairs split the key blocks (every case above);
-    # these two have 512 and keep 256-query workgroups
-    (2, 300, 128, 16, 64, True),   # ragged, GQA 8:1
-    (1, 264, 256, 64, 64, False),  # non-causal, ragged
+    # Launch shapes.  dQ: under 512 workgroups of 256 queries, 128-query
+    # workgroups whose wave pairs split the key blocks (every case above).
+    # dK/dV: MHA under 512 workgroups of 256 keys takes 128-key workgroups
+    # whose wave pairs split the query halves; under 512 workgroups of the
+    # chosen tile, workspace shares (every case above).
+    (2, 300, 128, 16, 64, True),   # dQ 256-query; dK/dV 256-key, 8 shares; GQA 8:1
+    (1, 264, 256, 256, 64, False), # 256-query and 256-key workgroups, non-causal, ragged
+    (1, 1000, 64, 64, 64, True),   # dK/dV 128-key, no shares (512 workgroups), ragged
 ]
 
 
