@@ -9,7 +9,10 @@
 //     issued longest-first (causal work grows with the query index), which
 //     balances the CUs without a persistent scheduler.  Register use stays
 //     under 256 per lane so that two workgroups share a CU (two waves per
-//     SIMD: one wave's softmax VALU work runs under the other's MFMAs);
+//     SIMD: one wave's softmax VALU work runs under the other's MFMAs).
+//     When the 128-query tiles would fill at most one round of the CUs' two
+//     workgroup slots (short sequences), tiles hold 64 queries instead and
+//     the wave pairs sharing a query group split each slice's key blocks;
 //   * each wave keeps its 32 queries' Q fragments in registers and computes
 //     S^T = K Q^T with 32x32x16 FP16 MFMA, so that every lane owns one query
 //     column: the row max and row sum are per-lane register reductions plus
@@ -37,6 +40,7 @@ constexpr int BKV = 64;      // keys per LDS slice
 constexpr int BQ = NW * 32;  // queries per workgroup
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLazy = 8.f; // log2 of the largest probability before a rescale
+constexpr int64_t kFwdSlots = 512;      // workgroup slots: two per CU
 
 template <int D>
 struct FwdSmem {
@@ -45,7 +49,13 @@ struct FwdSmem {
   static constexpr int STAGE = 2 * TILE;          // K then V
 };
 
-template <int D>
+// QSPLIT = 1: 4 query groups of 32 (128 queries); every wave walks both
+// 32-key blocks of each slice.  QSPLIT = 2 (short sequences, for twice the
+// workgroups): 2 query groups (64 queries); waves w and w + 2 share a query
+// group and take one 32-key block of each slice each, keeping their own
+// running max, row sum and O; the pair's states are merged through LDS at
+// the end (rescaled to the larger max, fixed order).
+template <int D, int QSPLIT>
 __global__ void __launch_bounds__(NW * 64, 2)
 attn_fwd_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
                 const lt_half* __restrict__ V, int64_t q_stride, int64_t kv_stride,
@@ -56,6 +66,12 @@ attn_fwd_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
   constexpr int KB = BKV / 32;     // 32-key blocks per slice
   constexpr int DB = D / 32;       // 32-feature blocks
   constexpr int KK = D / 16;       // MFMA steps over the head dim
+  constexpr int NQG = NW / QSPLIT;                 // query groups of 32
+  constexpr int BQW = NQG * 32;                    // queries per workgroup
+  constexpr int KBW = KB / QSPLIT;                 // 32-key blocks per slice and wave
+  static_assert(NW % QSPLIT == 0 && KB % QSPLIT == 0, "QSPLIT must divide waves and blocks");
+  static_assert(QSPLIT == 1 || NQG * DB * 4 * 64 * 16 + NQG * 64 * 8 <= 2 * SM::STAGE,
+                "merge fits in LDS");
   __shared__ __attribute__((aligned(1024))) char smem[2 * SM::STAGE];
 
   const int tid = threadIdx.x;
@@ -63,15 +79,17 @@ attn_fwd_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: scalar addressing
   const int lrow = lane & 31;
   const int g = lane >> 5;
+  const int qg = wave % NQG;                       // query group
+  const int kpart = wave / NQG;                    // which block of each slice (QSPLIT = 2)
 
-  const int n_qt = (S + BQ - 1) / BQ;
+  const int n_qt = (S + BQW - 1) / BQW;
   const int bh = blockIdx.x % (B * Hq);
   const int qt = causal ? n_qt - 1 - (int)(blockIdx.x / (B * Hq)) : (int)(blockIdx.x / (B * Hq));
   const int b = bh / Hq;
   const int h = bh % Hq;
   const int kvh = h / (Hq / Hkv);
-  const int q0 = qt * BQ;
-  const int qw0 = q0 + wave * 32;
+  const int q0 = qt * BQW;
+  const int qw0 = q0 + qg * 32;
   const int myq = qw0 + lrow;                      // query owned by this lane
 
   const lt_half* Kp = K + (int64_t)b * S * kv_stride + (int64_t)kvh * D;
@@ -97,7 +115,7 @@ attn_fwd_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
   float m_run = -INFINITY;   // running max (score units) used as the exponent offset
   float lsum = 0.f;          // this lane's share of the row sum
 
-  const int kv_end = causal ? min(S, q0 + BQ) : S;
+  const int kv_end = causal ? min(S, q0 + BQW) : S;
   const int n_kv = (kv_end + BKV - 1) / BKV;
   const int q_hi = min(qw0 + 32, S) - 1;           // last valid query of this wave
 
@@ -125,48 +143,52 @@ attn_fwd_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
     if (kt + 1 < n_kv) stage_load(kt + 1, (kt + 1) & 1);
 
     const int key0 = kt * BKV;
-    const bool active = (!causal || key0 <= q_hi) && qw0 < S;
+    // QSPLIT = 2: this wave's block, skipped when wholly above its queries
+    // or past S, so that every processed block has a visible key in every
+    // valid row (the running max stays finite)
+    const int kb0 = QSPLIT > 1 ? kpart * 32 : 0;
+    const bool active = (!causal || key0 + kb0 <= q_hi) && qw0 < S && key0 + kb0 < S;
     if (active) {
-      // ---- S^T = K Q^T ----
-      f32x16 sacc[KB];
+      // ---- S^T = K Q^T ----  (local block i is the slice's block kb0/32 + i)
+      f32x16 sacc[KBW];
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
+      for (int kb = 0; kb < KBW; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
       // K fragments of step kk+1 are read before the MFMAs of step kk
-      half8 kfr[KB];
+      half8 kfr[KBW];
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) kfr[kb] = RT::row_frag(st, kb * 32, 0, lane);
+      for (int kb = 0; kb < KBW; ++kb) kfr[kb] = RT::row_frag(st, kb0 + kb * 32, 0, lane);
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
-        half8 nxt[KB];
+        half8 nxt[KBW];
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
-          nxt[kb] = kk + 1 < KK ? RT::row_frag(st, kb * 32, kk + 1, lane) : kfr[kb];
+        for (int kb = 0; kb < KBW; ++kb)
+          nxt[kb] = kk + 1 < KK ? RT::row_frag(st, kb0 + kb * 32, kk + 1, lane) : kfr[kb];
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) sacc[kb] = mfma32(kfr[kb], qf[kk], sacc[kb]);
+        for (int kb = 0; kb < KBW; ++kb) sacc[kb] = mfma32(kfr[kb], qf[kk], sacc[kb]);
         if (kk + 1 < KK) {
-          __builtin_amdgcn_sched_group_barrier(0x100, KB, 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, KB, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, KBW, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, KBW, 0);
         }
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) kfr[kb] = nxt[kb];
+        for (int kb = 0; kb < KBW; ++kb) kfr[kb] = nxt[kb];
       }
 
       // ---- mask (key > query, or key past S), row max ----
       if ((causal && key0 + BKV - 1 > qw0) || key0 + BKV > S) {   // wave-uniform
         const int klim = causal ? min(myq + 1, S) : S;             // keys < klim are visible
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
+        for (int kb = 0; kb < KBW; ++kb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int key = key0 + kb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
+            const int key = key0 + kb0 + kb * 32 + 8 * (r >> 2) + 4 * g + (r & 3);
             sacc[kb][r] = key < klim ? sacc[kb][r] : -INFINITY;
           }
       }
       float mx = -INFINITY;
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
+      for (int kb = 0; kb < KBW; ++kb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kb][r]);
       mx = fmaxf(mx, __shfl_xor(mx, 32));
@@ -186,9 +208,9 @@ attn_fwd_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
 
       // ---- P = exp2(s c - m c), row sum, FP16 P^T fragments ----
       const float mc = m_run * c;
-      half8 pf[KB][2];
+      half8 pf[KBW][2];
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) {
+      for (int kb = 0; kb < KBW; ++kb) {
         float p[16];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
@@ -204,18 +226,57 @@ attn_fwd_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
       // ---- O^T += V^T P^T (V^T read transposed, keys in accumulator order) ----
       const char* vs = st + SM::TILE;
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
+      for (int kb = 0; kb < KBW; ++kb)
 #pragma unroll
         for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
           for (int db = 0; db < DB; ++db)
-            oacc[db] = mfma32(RT::template tr_frag<true>(vs, kb * 32 + kc * 16, db * 32, lane),
-                              pf[kb][kc], oacc[db]);
+            oacc[db] = mfma32(
+                RT::template tr_frag<true>(vs, kb0 + kb * 32 + kc * 16, db * 32, lane),
+                pf[kb][kc], oacc[db]);
     }
 
     // next slice resident for every wave; nobody reads this stage any more
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+  }
+
+  if constexpr (QSPLIT > 1) {
+    // every stage is free after the loop's last barrier: the second wave of
+    // each pair passes O (lane-major float4), its running max and row-sum
+    // share to the first, which rescales both to the larger max and adds
+    float4* red = reinterpret_cast<float4*>(smem);
+    float2* ml = reinterpret_cast<float2*>(smem + NQG * DB * 4 * 64 * 16);
+    if (kpart == 1) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int rq = 0; rq < 4; ++rq)
+          red[((qg * DB + db) * 4 + rq) * 64 + lane] =
+              make_float4(oacc[db][4 * rq], oacc[db][4 * rq + 1], oacc[db][4 * rq + 2],
+                          oacc[db][4 * rq + 3]);
+      ml[qg * 64 + lane] = make_float2(m_run, lsum);
+    }
+    __syncthreads();
+    if (kpart != 0) return;
+    const float2 o2 = ml[qg * 64 + lane];
+    const float m = fmaxf(m_run, o2.x);
+    // a wave that processed no block has m_run = -inf, a zero row sum and O;
+    // both -inf only for rows past S (never stored)
+    const float a1 = m == -INFINITY ? 0.f : fast_exp2((m_run - m) * c);
+    const float a2 = m == -INFINITY ? 0.f : fast_exp2((o2.x - m) * c);
+    m_run = m;
+    lsum = lsum * a1 + o2.y * a2;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        const float4 v = red[((qg * DB + db) * 4 + rq) * 64 + lane];
+        oacc[db][4 * rq] = oacc[db][4 * rq] * a1 + v.x * a2;
+        oacc[db][4 * rq + 1] = oacc[db][4 * rq + 1] * a1 + v.y * a2;
+        oacc[db][4 * rq + 2] = oacc[db][4 * rq + 2] * a1 + v.z * a2;
+        oacc[db][4 * rq + 3] = oacc[db][4 * rq + 3] * a1 + v.w * a2;
+      }
   }
 
   // ---- normalise and store O, LSE ----
@@ -241,11 +302,21 @@ attn_fwd_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
 template <int D>
 hipError_t launch_fwd(const AttnFwdArgs& a, hipStream_t s) {
   const AttnShape& sh = a.sh;
-  const int n_qt = (sh.S + BQ - 1) / BQ;
-  const dim3 grid((unsigned)(n_qt * sh.B * sh.Hq));
-  hipLaunchKernelGGL((attn_fwd_kernel<D>), grid, dim3(NW * 64), 0, s, a.Q, a.K, a.V,
-                     a.q_stride, a.kv_stride, a.O, a.o_stride, a.LSE, sh.B, sh.S, sh.Hq, sh.Hkv,
-                     sh.scale, sh.causal);
+  // 64-query workgroups when 128-query ones would fill at most one round of
+  // the slots (short sequences); with more, the split's extra K/V loads per
+  // MFMA cost more than the finer balance gains
+  const int64_t wgs128 = (int64_t)((sh.S + BQ - 1) / BQ) * sh.B * sh.Hq;
+  if (wgs128 > kFwdSlots) {
+    const dim3 grid((unsigned)wgs128);
+    hipLaunchKernelGGL((attn_fwd_kernel<D, 1>), grid, dim3(NW * 64), 0, s, a.Q, a.K, a.V,
+                       a.q_stride, a.kv_stride, a.O, a.o_stride, a.LSE, sh.B, sh.S, sh.Hq,
+                       sh.Hkv, sh.scale, sh.causal);
+  } else {
+    const dim3 grid((unsigned)((int64_t)((sh.S + BQ / 2 - 1) / (BQ / 2)) * sh.B * sh.Hq));
+    hipLaunchKernelGGL((attn_fwd_kernel<D, 2>), grid, dim3(NW * 64), 0, s, a.Q, a.K, a.V,
+                       a.q_stride, a.kv_stride, a.O, a.o_stride, a.LSE, sh.B, sh.S, sh.Hq,
+                       sh.Hkv, sh.scale, sh.causal);
+  }
   return hipGetLastError();
 }
 

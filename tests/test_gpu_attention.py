@@ -131,13 +131,15 @@ CASES = [
     (1, 384, 8, 2, 128, True),     # several tiles of every kernel
     (1, 130, 4, 4, 64, False),     # non-causal, ragged
     (2, 256, 4, 1, 128, False),    # non-causal, MQA
-    # Launch shapes.  dQ: under 512 workgroups of 256 queries, 128-query
-    # workgroups whose wave pairs split the key blocks (every case above).
-    # dK/dV: MHA under 512 workgroups of 256 keys takes 128-key workgroups
-    # whose wave pairs split the query halves; under 512 workgroups of the
-    # chosen tile, workspace shares (every case above).
-    (2, 300, 128, 16, 64, True),   # dQ 256-query; dK/dV 256-key, 8 shares; GQA 8:1
-    (1, 264, 256, 256, 64, False), # 256-query and 256-key workgroups, non-causal, ragged
+    # Launch shapes.  Forward: at most 512 workgroups of 128 queries, 64-query
+    # workgroups whose wave pairs split the key blocks.  dQ: under 512
+    # workgroups of 256 queries, 128-query workgroups whose wave pairs split
+    # the key blocks.  dK/dV: MHA under 512 workgroups of 256 keys takes
+    # 128-key workgroups whose wave pairs split the query halves; under 512
+    # workgroups of the chosen tile, workspace shares.  Every case above
+    # takes the split forward and dQ.
+    (2, 300, 256, 32, 64, True),   # fwd 128-query, dQ 256-query, dK/dV 256-key 4 shares; GQA 8:1
+    (1, 264, 256, 256, 64, False), # fwd 128-query, dQ 256-query, dK/dV 256-key, non-causal
     (1, 1000, 64, 64, 64, True),   # dK/dV 128-key, no shares (512 workgroups), ragged
 ]
 
