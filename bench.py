@@ -134,7 +134,8 @@ def sweep():
     * the paper's representative GEMM shapes (Sec. 6.6, Table "Representative
       FP16 GEMM backend profile", sequence length 2048): M = 2048 tokens,
       K x N = 4096x4096, 4096x11008, 11008x4096, 6656x6656, 8192x8192, as the
-      forward projection C = X W^T;
+      forward projection C = X W^T through lt_gemm_f16_ws with the split-K
+      workspace the library asks for (the call the layer makes);
     * the whole LLaMA-2-7B-shaped layer step at S = 1024 and 2048.
 
     Inputs are seeded normal tensors made on the device (timing only).
@@ -196,11 +197,15 @@ def sweep():
     for K, N in [(4096, 4096), (4096, 11008), (11008, 4096), (6656, 6656), (8192, 8192)]:
         A, Wt = rand(M, K), rand(N, K, std=0.02)
         C = torch.empty(M, N, dtype=torch.float16, device="cuda")
-        t = timed(lambda: lt.lt_gemm_f16(0, 1, M, N, K, 1.0, A, K, Wt, K, 0.0, C, N), iters=20)
+        gwb = lt.lt_gemm_f16_workspace_size(0, 1, M, N, K)
+        gws = torch.empty(gwb, dtype=torch.uint8, device="cuda") if gwb else None
+        t = timed(lambda: lt.lt_gemm_f16_ws(0, 1, M, N, K, 1.0, A, K, Wt, K, 0.0, None, N, None, C,
+                                            N, gws, gwb), iters=20)
         tfl = 2 * M * N * K / t / 1e9
         emit({"sweep": "gemm", "M": M, "K": K, "N": N, "layout": "NT (X W^T)", "ms": round(t, 4),
-              "tflops": round(tfl, 1), "frac_peak": round(tfl / PEAK_FP16_TFLOPS, 4)})
-        del A, Wt, C
+              "tflops": round(tfl, 1), "frac_peak": round(tfl / PEAK_FP16_TFLOPS, 4),
+              "split_k_workspace_mib": round(gwb / 2**20, 1)})
+        del A, Wt, C, gws
 
     base = WORKLOADS["llama2-7b"]
     for S in (1024, 2048):
