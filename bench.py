@@ -81,9 +81,13 @@ def layer_flops(w):
 def cpu_baseline(w, budget_s=20.0):
     """Time the float64 oracle on a bounded sample of the same workload.
 
-    Sample: the first R = 1024 rows of every one of the 12 GEMMs (about 10 s
-    on a 16-core host; the loop stops early past `budget_s`) plus one full
-    attention head forward and backward at the workload's sequence length.
+    Sample: the first R = min(4096, T) rows of every one of the 12 GEMMs (at
+    LLaMA-2-7B every row except in the gate/up and QKV weight gradients,
+    whose M is 22016 and 12288: 4.11 of the step's 4.97 TFLOP) and then whole causal
+    attention heads, forward and backward at the workload's sequence length,
+    one after another until the time passes `budget_s` or every query head
+    is done (all of them = the whole layer step at T = 4096).  At least one
+    head always runs; the GEMM loop also stops early past `budget_s`.
     Rate = algorithmic FLOPs of the sample / wall time.
     """
     import oracle
@@ -94,7 +98,7 @@ def cpu_baseline(w, budget_s=20.0):
     except Exception:
         cores = os.cpu_count() or 1
     T = w.T
-    R = min(1024, T)
+    R = min(4096, T)
     shapes = [(T, w.qkv_cols, w.H), (T, w.H, w.Hq * w.D), (T, 2 * w.F, w.H), (T, w.H, w.F),
               (w.H, w.F, T), (T, w.F, w.H), (2 * w.F, w.H, T), (T, w.H, 2 * w.F),
               (w.H, w.Hq * w.D, T), (T, w.Hq * w.D, w.H), (w.qkv_cols, w.H, T), (T, w.H, w.qkv_cols)]
@@ -110,19 +114,24 @@ def cpu_baseline(w, budget_s=20.0):
         if t_total > budget_s:
             break
     S, D = w.S, w.D
-    q = normal_f16(90200, (S, D)); k = normal_f16(90201, (S, D))
-    v = normal_f16(90202, (S, D)); do = normal_f16(90203, (S, D))
-    t0 = time.perf_counter()
-    oracle.attn_head_fwd(q, k, v, 1 / math.sqrt(D), True)
-    oracle.attn_head_bwd(q, k, v, do, 1 / math.sqrt(D), True)
-    t_total += time.perf_counter() - t0
     pairs = S * (S + 1) // 2
-    flops += 6 * 2 * D * pairs
+    heads = 0
+    for hh in range(w.Hq):
+        q = normal_f16(90200 + 4 * hh, (S, D)); k = normal_f16(90201 + 4 * hh, (S, D))
+        v = normal_f16(90202 + 4 * hh, (S, D)); do = normal_f16(90203 + 4 * hh, (S, D))
+        t0 = time.perf_counter()
+        oracle.attn_head_fwd(q, k, v, 1 / math.sqrt(D), True)
+        oracle.attn_head_bwd(q, k, v, do, 1 / math.sqrt(D), True)
+        t_total += time.perf_counter() - t0
+        flops += 6 * 2 * D * pairs
+        heads += 1
+        if t_total > budget_s:
+            break
     return {"value": flops / t_total / 1e12, "unit": "TFLOP/s", "cores": int(cores),
             "kind": "oracle",
-            "sample": (f"{w.name}: first {R} rows of each of the 12 layer GEMMs + one full causal "
-                       f"attention head fwd+bwd (S={S}, d={D}); {flops / 1e9:.1f} GFLOP in "
-                       f"{t_total:.1f} s, float64 numpy/OpenBLAS")}
+            "sample": (f"{w.name}: first {R} rows of each of the 12 layer GEMMs + {heads} of "
+                       f"{w.Hq} causal attention heads fwd+bwd (S={S}, d={D}); "
+                       f"{flops / 1e9:.1f} GFLOP in {t_total:.1f} s, float64 numpy/OpenBLAS")}
 
 
 def sweep():
