@@ -141,6 +141,8 @@ CASES = [
     (2, 300, 256, 32, 64, True),   # fwd 128-query, dQ 256-query, dK/dV 256-key 4 shares; GQA 8:1
     (1, 264, 256, 256, 64, False), # fwd 128-query, dQ 256-query, dK/dV 256-key, non-causal
     (1, 1000, 64, 64, 64, True),   # dK/dV 128-key, no shares (512 workgroups), ragged
+    (2, 200, 4, 4, 128, True),     # MHA, batch 2, ragged: every split form with shares
+    (2, 160, 2, 2, 128, False),    # the same, non-causal
 ]
 
 
