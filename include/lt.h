@@ -136,9 +136,11 @@ lt_status lt_gemm_f16_bias(int transA, int transB, int64_t M, int64_t N,
  *
  *   Same conventions and errors as lt_gemm_f16_res; bias may be NULL (no
  *   bias), else [N] FP16, 16-byte aligned.  The workspace lets the kernel
- *   split the reduction (K) of the tiles of a last, at most half full, wave
- *   of output tiles over several workgroups: their FP32 partial sums go to
- *   the workspace and are added in a fixed order (deterministic) before the
+ *   split the reduction (K) of output tiles over several workgroups: the
+ *   tiles of a last, at most half full, wave of 256x256 tiles, or all tiles
+ *   of a launch of less than about one wave when the split gives 8 shares or
+ *   keeps at least 2048 of K per share.  Their FP32 partial sums go to the
+ *   workspace and are added in a fixed order (deterministic) before the
  *   single rounding of C.  The result can differ from lt_gemm_f16_res in the
  *   last bits of those tiles (another FP32 summation order).
  *   workspace: device memory owned by the caller, 16-byte aligned (else
