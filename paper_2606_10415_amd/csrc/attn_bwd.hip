@@ -7,9 +7,9 @@
 // Here P is rebuilt from the forward's row LSE, P = exp(scale q.k - LSE), and
 // SoftmaxBackward is GS = P * (GP - D) with D_i = rowsum(GO_i * O_i).
 //
-// Three kernels (four with grouped queries), none with an atomic:
-//   1. attn_bwd_pre : D_i = rowsum(dO_i * O_i) (one 8/16-lane group per row,
-//                     shuffle reduction) and the LSE in base 2.  HBM-bound.
+// Two kernels (three with workspace shares), none with an atomic, launched
+// dQ first because it also forms D_i = rowsum(dO_i * O_i) and the LSE in
+// base 2 for its queries and stores them for the dK/dV pass:
 //   2. attn_bwd_dkdv: key-major.  One workgroup per (batch, kv head, 256-key
 //                     tile); each of the 8 waves owns 32 keys and keeps their
 //                     K fragments and the dK, dV accumulators in registers for
@@ -30,8 +30,8 @@
 //                     (query head, query block) work is split over several
 //                     workgroups, whose FP32 partial dK, dV go to the
 //                     workspace and are summed in a fixed order by
-//                     attn_bwd_dkdv_sum (kernel 4).
-//   3. attn_bwd_dq  : query-major, the forward's layout.  One workgroup per
+//                     attn_bwd_dkdv_sum (kernel 3).
+//   1. attn_bwd_dq  : query-major, the forward's layout.  One workgroup per
 //                     (batch, head, 256-query tile, 8 waves); each wave owns 32 queries
 //                     (Q and dO fragments and the dQ accumulator in registers)
 //                     and walks the causal 128-key slices of K and V (direct
@@ -45,7 +45,7 @@
 //                     end, which doubles the workgroups and halves the
 //                     longest causal tile.  Key blocks wholly above a wave's
 //                     queries are skipped.
-// Kernels 2 and 3 both recompute S and dP: seven contractions instead of
+// Kernels 1 and 2 both recompute S and dP: seven contractions instead of
 // five, traded for no dQ atomics (whose traffic would exceed the whole
 // algorithmic byte count several times) and two waves per SIMD in each.
 
@@ -65,41 +65,7 @@ constexpr int BKB = 128;       // dQ: keys per slice
 constexpr int64_t kDqFillWgs = 512;   // dQ: 256-query workgroups needed to skip the split
 constexpr float kLog2e = 1.4426950408889634f;
 
-// ------------------------------------------------------------ kernel 1
-template <int D>
-__global__ void __launch_bounds__(256)
-attn_bwd_pre_kernel(const lt_half* __restrict__ O, const lt_half* __restrict__ dO, int64_t o_stride,
-                    const float* __restrict__ LSE, float* __restrict__ delta,
-                    float* __restrict__ lse2, int B, int S, int Hq) {
-  constexpr int LPR = D / 8;                       // lanes per row
-  const int64_t rows = (int64_t)B * S * Hq;
-  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t row = gid / LPR;
-  const int part = (int)(gid % LPR);
-  float s = 0.f;
-  if (row < rows) {
-    const int h = (int)(row % Hq);
-    const int64_t bi = row / Hq;                   // b*S + i
-    const int64_t off = bi * o_stride + (int64_t)h * D + part * 8;
-    const half8 o = as_half8(ld16(O + off));
-    const half8 d = as_half8(ld16(dO + off));
-#pragma unroll
-    for (int e = 0; e < 8; ++e) s += (float)o[e] * (float)d[e];
-  }
-#pragma unroll
-  for (int m = LPR / 2; m >= 1; m >>= 1) s += __shfl_xor(s, m);
-  if (row < rows && part == 0) {
-    const int h = (int)(row % Hq);
-    const int64_t bi = row / Hq;
-    const int64_t b = bi / S;
-    const int64_t i = bi % S;
-    const int64_t idx = (b * Hq + h) * S + i;
-    delta[idx] = s;
-    lse2[idx] = LSE[idx] * kLog2e;
-  }
-}
-
-// ------------------------------------------------------------ kernel 2
+// ------------------------------------------------------------ kernel 2: dK/dV
 template <int D>
 struct DkdvSmem {
   using RT = RowTile<D, NWA>;
@@ -401,7 +367,7 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
   }
 }
 
-// ------------------------------------------------------------ kernel 3
+// ------------------------------------------------------------ kernel 1: dQ (and D)
 template <int D>
 struct DqSmem {
   using RT = RowTile<D, NW>;
@@ -418,8 +384,9 @@ template <int D, int QSPLIT>
 __global__ void __launch_bounds__(NW * 64, 2)
 attn_bwd_dq_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
                    const lt_half* __restrict__ V, int64_t q_stride, int64_t kv_stride,
-                   const lt_half* __restrict__ dO, int64_t o_stride, const float* __restrict__ lse2,
-                   const float* __restrict__ delta, lt_half* __restrict__ dQ, int64_t dq_stride,
+                   const lt_half* __restrict__ O, const lt_half* __restrict__ dO, int64_t o_stride,
+                   const float* __restrict__ LSE, float* __restrict__ lse2,
+                   float* __restrict__ delta, lt_half* __restrict__ dQ, int64_t dq_stride,
                    int B, int S, int Hq, int Hkv, float scale, int causal) {
   using SM = DqSmem<D>;
   using RT = RowTile<D, NW>;
@@ -455,26 +422,28 @@ attn_bwd_dq_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
   const float c = scale * kLog2e;
 
   // Q and dO fragments (B operands of S^T = K Q^T and dP^T = V dO^T):
-  // column = this lane's query, reduction indices kk*16 + 8g + 0..7.
-  // Queries past S: zero Q, dO, LSE2 and D give zero dS.
-  half8 qf[KK], of[KK];
+  // column = this lane's query, reduction indices kk*16 + 8g + 0..7; the
+  // same half-row of O for D.  Queries past S: zero Q, dO, O and LSE2 give
+  // zero dS.
+  half8 qf[KK], of[KK], oo[KK];
   float l2 = 0.f, dl = 0.f;
+  const int64_t ri = ((int64_t)b * Hq + h) * S + myq;   // [B, Hq, S] row entry
   if (myq < S) {
     const lt_half* qp = Q + ((int64_t)b * S + myq) * q_stride + (int64_t)h * D + g * 8;
-    const lt_half* op = dO + ((int64_t)b * S + myq) * o_stride + (int64_t)h * D + g * 8;
+    const int64_t orow = ((int64_t)b * S + myq) * o_stride + (int64_t)h * D + g * 8;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       qf[kk] = as_half8(ld16(qp + kk * 16));
-      of[kk] = as_half8(ld16(op + kk * 16));
+      of[kk] = as_half8(ld16(dO + orow + kk * 16));
+      oo[kk] = as_half8(ld16(O + orow + kk * 16));
     }
-    const int64_t ri = ((int64_t)b * Hq + h) * S + myq;
-    l2 = lse2[ri];
-    dl = delta[ri];
+    l2 = LSE[ri] * kLog2e;
   } else {
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       qf[kk] = as_half8(u32x4{0, 0, 0, 0});
       of[kk] = as_half8(u32x4{0, 0, 0, 0});
+      oo[kk] = as_half8(u32x4{0, 0, 0, 0});
     }
   }
 
@@ -504,9 +473,24 @@ attn_bwd_dq_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
   for (int kk = 0; kk < KK; ++kk) {
     loaded_here(qf[kk]);
     loaded_here(of[kk]);
+    loaded_here(oo[kk]);
   }
   loaded_here(l2);
-  loaded_here(dl);
+  // D_i = rowsum(dO_i * O_i): this lane's half of the row, then its
+  // partner's (lanes l and l ^ 32 own the same query).  The first wave of
+  // each query group stores D and the base-2 LSE for the dK/dV kernel.
+  {
+    float part = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) part = fmaf((float)of[kk][e], (float)oo[kk][e], part);
+    dl = part + __shfl_xor(part, 32);
+  }
+  if (myq < S && g == 0 && kpart == 0) {
+    delta[ri] = dl;
+    lse2[ri] = l2;
+  }
 
   for (int kt = 0; kt < n_kv; ++kt) {
     const char* ks = smem + (kt & 1) * SM::STAGE;
@@ -613,7 +597,7 @@ attn_bwd_dq_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
   }
 }
 
-// ------------------------------------------------------------ kernel 4
+// ------------------------------------------------------------ kernel 3: dK/dV share sum
 // Grouped queries split over several dK/dV workgroups: dK = scale * sum of
 // the FP32 partials, dV = sum, in split order (deterministic).  HBM-bound.
 template <int D>
@@ -651,11 +635,22 @@ attn_bwd_dkdv_sum_kernel(const float* __restrict__ part, int nsplit, lt_half* __
 template <int D>
 hipError_t launch_bwd(const AttnBwdArgs& a, hipStream_t s) {
   const AttnShape& sh = a.sh;
-  const int64_t rows = (int64_t)sh.B * sh.S * sh.Hq;
-  const int64_t threads = rows * (D / 8);
-  const unsigned eblocks = (unsigned)((threads + 255) / 256);
-  hipLaunchKernelGGL((attn_bwd_pre_kernel<D>), dim3(eblocks), dim3(256), 0, s, a.O, a.dO,
-                     a.o_stride, a.LSE, a.delta, a.lse2, sh.B, sh.S, sh.Hq);
+  // dQ first: it also writes D and the base-2 LSE that the dK/dV pass reads.
+  // 256-query workgroups while they give at least two per CU, else 128.
+  const int64_t wgs256 = (int64_t)((sh.S + BQB - 1) / BQB) * sh.B * sh.Hq;
+  if (wgs256 >= kDqFillWgs) {
+    const int n_qt = (sh.S + BQB - 1) / BQB;
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<D, 1>), dim3((unsigned)(n_qt * sh.B * sh.Hq)),
+                       dim3(NW * 64), 0, s, a.Q, a.K, a.V, a.q_stride, a.kv_stride, a.O, a.dO,
+                       a.o_stride, a.LSE, a.lse2, a.delta, a.dQ, a.dq_stride, sh.B, sh.S, sh.Hq,
+                       sh.Hkv, sh.scale, sh.causal);
+  } else {
+    const int n_qt = (sh.S + BQB / 2 - 1) / (BQB / 2);
+    hipLaunchKernelGGL((attn_bwd_dq_kernel<D, 2>), dim3((unsigned)(n_qt * sh.B * sh.Hq)),
+                       dim3(NW * 64), 0, s, a.Q, a.K, a.V, a.q_stride, a.kv_stride, a.O, a.dO,
+                       a.o_stride, a.LSE, a.lse2, a.delta, a.dQ, a.dq_stride, sh.B, sh.S, sh.Hq,
+                       sh.Hkv, sh.scale, sh.causal);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int n_kt = (sh.S + a.ktile - 1) / a.ktile;
@@ -680,24 +675,8 @@ hipError_t launch_bwd(const AttnBwdArgs& a, hipStream_t s) {
                        dim3(256), 0, s, a.part, a.nsplit, a.dK, a.dV, a.dkv_stride, sh.B, sh.S,
                        sh.Hkv, sh.scale);
     e = hipGetLastError();
-    if (e != hipSuccess) return e;
   }
-  // 256-query workgroups while they give at least two per CU, else 128
-  const int64_t wgs256 = (int64_t)((sh.S + BQB - 1) / BQB) * sh.B * sh.Hq;
-  if (wgs256 >= kDqFillWgs) {
-    const int n_qt = (sh.S + BQB - 1) / BQB;
-    hipLaunchKernelGGL((attn_bwd_dq_kernel<D, 1>), dim3((unsigned)(n_qt * sh.B * sh.Hq)),
-                       dim3(NW * 64), 0, s, a.Q, a.K, a.V, a.q_stride, a.kv_stride, a.dO,
-                       a.o_stride, a.lse2, a.delta, a.dQ, a.dq_stride, sh.B, sh.S, sh.Hq, sh.Hkv,
-                       sh.scale, sh.causal);
-  } else {
-    const int n_qt = (sh.S + BQB / 2 - 1) / (BQB / 2);
-    hipLaunchKernelGGL((attn_bwd_dq_kernel<D, 2>), dim3((unsigned)(n_qt * sh.B * sh.Hq)),
-                       dim3(NW * 64), 0, s, a.Q, a.K, a.V, a.q_stride, a.kv_stride, a.dO,
-                       a.o_stride, a.lse2, a.delta, a.dQ, a.dq_stride, sh.B, sh.S, sh.Hq, sh.Hkv,
-                       sh.scale, sh.causal);
-  }
-  return hipGetLastError();
+  return e;
 }
 
 }  // namespace
