@@ -46,8 +46,8 @@ GEMM_TRAFFIC = {
     "layer": "paper",
     "fuse_swiglu": True,
     "sources_sha256": "c4d454f978e0802ef87dd5dcb1d6886726658401e62d0402a4a84ec4f793d469",
-    "fetch_bytes_per_launch": 664189724,
-    "write_bytes_per_launch": 100034425,
+    "fetch_bytes_per_launch": 664103038,
+    "write_bytes_per_launch": 99974501,
 }
 GEMM_SOURCES = ("paper_2606_10415_amd/csrc/gemm_f16.hip", "paper_2606_10415_amd/csrc/common.hpp")
 
