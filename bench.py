@@ -78,6 +78,20 @@ def layer_flops(w):
             "total": 3 * gemm_fwd + attn_fwd + attn_bwd}
 
 
+def host_cpu_model():
+    """The host CPU's model name (first entry of /proc/cpuinfo) and logical CPU count."""
+    name = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return f"{name} ({os.cpu_count()} logical CPUs visible)"
+
+
 def cpu_baseline(w, budget_s=20.0):
     """Time the float64 oracle on a bounded sample of the same workload.
 
@@ -128,7 +142,7 @@ def cpu_baseline(w, budget_s=20.0):
         if t_total > budget_s:
             break
     return {"value": flops / t_total / 1e12, "unit": "TFLOP/s", "cores": int(cores),
-            "kind": "oracle",
+            "cpu": host_cpu_model(), "kind": "oracle",
             "sample": (f"{w.name}: first {R} rows of each of the 12 layer GEMMs + {heads} of "
                        f"{w.Hq} causal attention heads fwd+bwd (S={S}, d={D}); "
                        f"{flops / 1e9:.1f} GFLOP in {t_total:.1f} s, float64 numpy/OpenBLAS")}

@@ -192,7 +192,9 @@ lt_status lt_bias_grad_f16(const lt_half* dY, int64_t lddy, int64_t T, int64_t N
  *   Errors: INVALID_ARG for NULL pointers, B/S/Hq/Hkv < 1, Hq % Hkv != 0,
  *   causal not 0/1, scale not finite and > 0, strides smaller than the row
  *   length;
- *   UNSUPPORTED for D not in {64, 128}, misaligned pointers or strides.
+ *   UNSUPPORTED for D not in {64, 128}, misaligned pointers or strides, or a
+ *   row stride of 2^22 elements or more (tiles are loaded with 32-bit byte
+ *   offsets).
  */
 lt_status lt_attn_fwd(const lt_half* Q, const lt_half* K, const lt_half* V,
                       int64_t q_row_stride, int64_t kv_row_stride, lt_half* O,
@@ -229,8 +231,9 @@ size_t lt_attn_bwd_workspace_size(int B, int S, int Hq, int Hkv, int D);
  *   overwritten.  `workspace` is a device buffer of at least
  *   lt_attn_bwd_workspace_size(...) bytes, 256-byte aligned, owned by the
  *   caller; its contents on entry are ignored.
- *   Errors: as lt_attn_fwd, plus LT_ERR_WORKSPACE if workspace is NULL or
- *   ws_bytes is too small.
+ *   Errors: as lt_attn_fwd (every row stride, dq_row_stride and
+ *   dkv_row_stride included, must be < 2^22 elements), plus LT_ERR_WORKSPACE
+ *   if workspace is NULL or ws_bytes is too small.
  */
 lt_status lt_attn_bwd(const lt_half* Q, const lt_half* K, const lt_half* V,
                       int64_t q_row_stride, int64_t kv_row_stride,

@@ -21,7 +21,7 @@ LIB = os.path.join(HERE, "liblt.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["lt_api.cpp", "gemm_f16.hip", "attn_fwd.hip", "attn_bwd.hip", "swiglu.hip", "norm_rope.hip",
+SOURCES = ["lt_api.cpp", "plan.cpp", "gemm_f16.hip", "attn_fwd.hip", "attn_bwd.hip", "swiglu.hip", "norm_rope.hip",
            "bias_grad.hip"]
 
 COMMON_FLAGS = [

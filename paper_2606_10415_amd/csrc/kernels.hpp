@@ -119,14 +119,15 @@ struct DkdvPlan {
 };
 inline DkdvPlan attn_bwd_dkdv_plan(int B, int S, int Hq, int Hkv) {
   const int grp = Hq / Hkv;
-  const int ktile = grp > 1 || (int64_t)((S + 255) / 256) * B * Hkv >= 512 ? 256 : 128;
-  const int n_kt = (S + ktile - 1) / ktile;
-  const int64_t wgs = (int64_t)n_kt * B * Hkv;
+  const int64_t S64 = S;
+  const int ktile = grp > 1 || ((S64 + 255) / 256) * B * Hkv >= 512 ? 256 : 128;
+  const int64_t n_kt = (S64 + ktile - 1) / ktile;
+  const int64_t wgs = n_kt * B * Hkv;
   if (wgs >= 512) return {ktile, 1};
   for (int n = 2; n <= grp; ++n)
     if (grp % n == 0 && wgs * n >= 512) return {ktile, n};
-  const int n_qb = (S + 63) / 64;
-  const int64_t last_pairs = (int64_t)grp * (n_qb - (int64_t)(n_kt - 1) * (ktile / 64));
+  const int64_t n_qb = (S64 + 63) / 64;
+  const int64_t last_pairs = (int64_t)grp * (n_qb - (n_kt - 1) * (ktile / 64));
   int64_t n = (kDkdvFillWgs + wgs - 1) / wgs;
   if (n < grp) n = grp;                                  // at least one share per query head
   if (n > 16) n = 16;
@@ -157,7 +158,7 @@ struct RmsBwdArgs {
 };
 constexpr int kRmsBwdWaves = 8;
 inline int rmsnorm_bwd_blocks(int64_t T) {   // about one row per wave, at most 512 workgroups
-  const int64_t b = (T + kRmsBwdWaves - 1) / kRmsBwdWaves;
+  const int64_t b = T / kRmsBwdWaves + (T % kRmsBwdWaves != 0);   // no overflow at any T
   return (int)(b < 512 ? (b < 1 ? 1 : b) : 512);
 }
 inline size_t rmsnorm_bwd_ws_bytes(int64_t T, int64_t H) {
@@ -166,7 +167,7 @@ inline size_t rmsnorm_bwd_ws_bytes(int64_t T, int64_t H) {
 
 // bias gradient (column sum): FP32 partial rows of the workspace
 inline int bias_grad_blocks(int64_t T) {
-  const int64_t b = (T + 63) / 64;
+  const int64_t b = T / 64 + (T % 64 != 0);
   return (int)(b < 128 ? (b < 1 ? 1 : b) : 128);
 }
 inline size_t bias_grad_ws_bytes(int64_t T, int64_t N) {

@@ -35,6 +35,15 @@ lt_status from_hip(hipError_t e, const char* what) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// B * S * Hq rows of the [B, Hq, S] row terms above 2^31 (checked without overflow)
+bool too_many_rows(int B, int S, int Hq) {
+  return (int64_t)B * S > (((int64_t)1 << 31) / Hq);
+}
+
+// Row tiles of up to 256 rows are loaded by buffer instructions with 32-bit
+// byte offsets: rows * stride * 2 bytes must stay below 2^31.
+constexpr int64_t kMaxAttnStride = (int64_t)1 << 22;
+
 lt_status check_attn_common(const void* Q, const void* K, const void* V, int64_t q_stride,
                             int64_t kv_stride, int B, int S, int Hq, int Hkv, int D, float scale,
                             int causal) {
@@ -53,10 +62,11 @@ lt_status check_attn_common(const void* Q, const void* K, const void* V, int64_t
   if (D != 64 && D != 128) return fail(LT_ERR_UNSUPPORTED, "head dim %d not in {64, 128}", D);
   if ((q_stride & 7) || (kv_stride & 7))
     return fail(LT_ERR_UNSUPPORTED, "row strides must be multiples of 8 elements");
+  if (q_stride >= kMaxAttnStride || kv_stride >= kMaxAttnStride)
+    return fail(LT_ERR_UNSUPPORTED, "q/kv row strides must be < 2^22 elements (32-bit buffer offsets)");
   if (!aligned16(Q) || !aligned16(K) || !aligned16(V))
     return fail(LT_ERR_UNSUPPORTED, "Q/K/V must be 16-byte aligned");
-  if ((int64_t)B * S * Hq > (int64_t)1 << 31)
-    return fail(LT_ERR_UNSUPPORTED, "B*S*Hq too large");
+  if (too_many_rows(B, S, Hq)) return fail(LT_ERR_UNSUPPORTED, "B*S*Hq too large");
   return LT_OK;
 }
 
@@ -153,7 +163,7 @@ lt_status lt_gemm_f16_ws(int transA, int transB, int64_t M, int64_t N, int64_t K
 }
 
 size_t lt_bias_grad_workspace_size(int64_t T, int64_t N) {
-  if (T < 1 || N < 1) return 0;
+  if (T < 1 || N < 1 || N > ((int64_t)1 << 40)) return 0;
   return lt::bias_grad_ws_bytes(T, N);
 }
 
@@ -194,6 +204,8 @@ lt_status lt_attn_fwd(const lt_half* Q, const lt_half* K, const lt_half* V, int6
   if (o_row_stride < (int64_t)Hq * D) return fail(LT_ERR_INVALID_ARG, "o_row_stride < Hq*D");
   if ((o_row_stride & 7) || !aligned16(O))
     return fail(LT_ERR_UNSUPPORTED, "O must be 16-byte aligned with stride % 8 == 0");
+  if (o_row_stride >= kMaxAttnStride)
+    return fail(LT_ERR_UNSUPPORTED, "o_row_stride must be < 2^22 elements");
   if (reinterpret_cast<uintptr_t>(LSE) & 3u) return fail(LT_ERR_UNSUPPORTED, "LSE must be 4-byte aligned");
   lt::AttnFwdArgs a{{B, S, Hq, Hkv, D, scale, causal}, Q, K, V, q_row_stride, kv_row_stride, O,
                     o_row_stride, LSE};
@@ -202,6 +214,7 @@ lt_status lt_attn_fwd(const lt_half* Q, const lt_half* K, const lt_half* V, int6
 
 size_t lt_attn_bwd_workspace_size(int B, int S, int Hq, int Hkv, int D) {
   if (B < 1 || S < 1 || Hq < 1 || Hkv < 1 || D < 1 || Hq % Hkv) return 0;
+  if (too_many_rows(B, S, Hq) || (D != 64 && D != 128)) return 0;   // lt_attn_bwd rejects these
   return lt::attn_bwd_delta_bytes(B, S, Hq) + lt::attn_bwd_lse2_bytes(B, S, Hq) +
          lt::attn_bwd_part_bytes(B, S, Hq, Hkv, D);
 }
@@ -222,6 +235,9 @@ lt_status lt_attn_bwd(const lt_half* Q, const lt_half* K, const lt_half* V, int6
     return fail(LT_ERR_INVALID_ARG, "o/dq/dkv row stride smaller than the row length");
   if ((o_row_stride | dq_row_stride | dkv_row_stride) & 7)
     return fail(LT_ERR_UNSUPPORTED, "row strides must be multiples of 8 elements");
+  if (o_row_stride >= kMaxAttnStride || dq_row_stride >= kMaxAttnStride ||
+      dkv_row_stride >= kMaxAttnStride)
+    return fail(LT_ERR_UNSUPPORTED, "o/dq/dkv row strides must be < 2^22 elements");
   if (!aligned16(O) || !aligned16(dO) || !aligned16(dQ) || !aligned16(dK) || !aligned16(dV))
     return fail(LT_ERR_UNSUPPORTED, "O/dO/dQ/dK/dV must be 16-byte aligned");
   if (reinterpret_cast<uintptr_t>(LSE) & 3u) return fail(LT_ERR_UNSUPPORTED, "LSE must be 4-byte aligned");
@@ -252,6 +268,8 @@ lt_status lt_gemm_gu_swiglu_f16(const lt_half* X, int64_t ldx, const lt_half* Wg
   if (T < 0 || H < 0 || F < 0) return fail(LT_ERR_INVALID_ARG, "negative size");
   if (T == 0 || F == 0) return ok();
   if (!X || !Wgu || !GU || !A) return fail(LT_ERR_INVALID_ARG, "NULL pointer");
+  if (T > (int64_t)1 << 30 || F > (int64_t)1 << 29 || H > (int64_t)1 << 30)
+    return fail(LT_ERR_UNSUPPORTED, "T, H or F too large for the tile grid");
   if (ldx < H || ldw < H || ldgu < 2 * F || lda < F)
     return fail(LT_ERR_INVALID_ARG, "row stride smaller than the row length");
   if ((T | H | F) & 7) return fail(LT_ERR_UNSUPPORTED, "T, H, F must be multiples of 8");
@@ -259,8 +277,6 @@ lt_status lt_gemm_gu_swiglu_f16(const lt_half* X, int64_t ldx, const lt_half* Wg
     return fail(LT_ERR_UNSUPPORTED, "leading dimensions must be multiples of 8");
   if (!aligned16(X) || !aligned16(Wgu) || !aligned16(GU) || !aligned16(A))
     return fail(LT_ERR_UNSUPPORTED, "X, Wgu, GU, A must be 16-byte aligned");
-  if (T > (int64_t)1 << 30 || F > (int64_t)1 << 29 || H > (int64_t)1 << 30)
-    return fail(LT_ERR_UNSUPPORTED, "T, H or F too large for the tile grid");
   if (ldx >= ((int64_t)1 << 22) || ldw >= ((int64_t)1 << 22) || 2 * F * ldw >= ((int64_t)1 << 30) - 128)
     return fail(LT_ERR_UNSUPPORTED, "operands too large for 32-bit buffer offsets");
   lt::GemmArgs g{0, 1, T, 2 * F, H, 1.f, 0.f, X, ldx, Wgu, ldw, GU, ldgu, GU, ldgu};
@@ -278,6 +294,8 @@ lt_status lt_gemm_swiglu_bwd_f16(const lt_half* dY, int64_t lddy, const lt_half*
   if (T < 0 || H < 0 || F < 0) return fail(LT_ERR_INVALID_ARG, "negative size");
   if (T == 0 || F == 0) return ok();
   if (!dY || !Wd || !GU || !dGU) return fail(LT_ERR_INVALID_ARG, "NULL pointer");
+  if (T > (int64_t)1 << 30 || F > (int64_t)1 << 30 || H > (int64_t)1 << 30)
+    return fail(LT_ERR_UNSUPPORTED, "T, H or F too large for the tile grid");
   if (lddy < H || ldwd < F || ldgu < 2 * F || lddgu < 2 * F)
     return fail(LT_ERR_INVALID_ARG, "row stride smaller than the row length");
   if ((T | H | F) & 7) return fail(LT_ERR_UNSUPPORTED, "T, H, F must be multiples of 8");
@@ -285,8 +303,6 @@ lt_status lt_gemm_swiglu_bwd_f16(const lt_half* dY, int64_t lddy, const lt_half*
     return fail(LT_ERR_UNSUPPORTED, "leading dimensions must be multiples of 8");
   if (!aligned16(dY) || !aligned16(Wd) || !aligned16(GU) || !aligned16(dGU))
     return fail(LT_ERR_UNSUPPORTED, "dY, Wd, GU, dGU must be 16-byte aligned");
-  if (T > (int64_t)1 << 30 || F > (int64_t)1 << 30 || H > (int64_t)1 << 30)
-    return fail(LT_ERR_UNSUPPORTED, "T, H or F too large for the tile grid");
   if (lddy >= ((int64_t)1 << 22) || ldwd >= ((int64_t)1 << 22))
     return fail(LT_ERR_UNSUPPORTED, "lddy/ldwd must be < 2^22 elements (32-bit buffer offsets)");
   lt::GemmArgs g{0, 0, T, F, H, 1.f, 0.f, dY, lddy, Wd, ldwd, dGU, lddgu, dGU, lddgu};
@@ -299,7 +315,8 @@ lt_status lt_gemm_swiglu_bwd_f16(const lt_half* dY, int64_t lddy, const lt_half*
 }
 
 size_t lt_rmsnorm_bwd_workspace_size(int64_t T, int64_t H) {
-  if (T < 1 || H < 1) return 0;
+  if (T < 1 || H < 1 || H > 8192) return 0;           // H above the supported row width
+
   return lt::rmsnorm_bwd_ws_bytes(T, H);
 }
 

@@ -43,3 +43,16 @@ def rel_f(x, ref):
     ref = np.asarray(ref, dtype=np.float64)
     den = np.linalg.norm(ref)
     return float(np.linalg.norm(x - ref) / (den if den > 0 else 1.0))
+
+
+def row_err(x, ref):
+    """Largest row error norm relative to the RMS row norm of ``ref``.
+
+    x, ref: [rows, features].  max_i ||x_i - ref_i|| / sqrt(mean_i ||ref_i||^2):
+    a per-row bound that a single wrong row cannot dilute, and that stays
+    meaningful for rows whose reference is exactly zero."""
+    x = np.asarray(x, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    rms = math.sqrt(float(np.mean(np.sum(ref * ref, axis=1))))
+    worst = float(np.max(np.linalg.norm(x - ref, axis=1)))
+    return worst / (rms if rms > 0 else 1.0)

@@ -93,6 +93,9 @@ def _fwd(**kw):
     (dict(D=96), lt.LT_ERR_UNSUPPORTED),
     (dict(qs=388), lt.LT_ERR_UNSUPPORTED),
     (dict(K=FAKE + 8), lt.LT_ERR_UNSUPPORTED),
+    (dict(qs=1 << 22), lt.LT_ERR_UNSUPPORTED),          # 32-bit buffer offsets of row tiles
+    (dict(kvs=1 << 22), lt.LT_ERR_UNSUPPORTED),
+    (dict(os=1 << 22), lt.LT_ERR_UNSUPPORTED),
 ])
 def test_attn_fwd_rejects_on_host(kw, status):
     assert _fwd(**kw) == status
@@ -140,6 +143,11 @@ def test_attn_bwd_workspace():
     assert st == lt.LT_ERR_WORKSPACE
     st = lt._lib.lt_attn_bwd(*args, FAKE + 16, ws, 2, 100, 8, 2, 128, 0.09, 1, None)
     assert st == lt.LT_ERR_WORKSPACE
+    for i in (3, 4, 7, 12, 13):                       # q, kv, o, dq, dkv row strides
+        big = list(args)
+        big[i] = 1 << 22
+        st = lt._lib.lt_attn_bwd(*big, FAKE, ws, 2, 100, 8, 2, 128, 0.09, 1, None)
+        assert st == lt.LT_ERR_UNSUPPORTED, i
 
 
 def test_swiglu_rejects_on_host():

@@ -3,6 +3,14 @@
 Bars (written here, derived in the design doc):
   O: relative Frobenius error <= 5e-3;  LSE: max abs error <= 1e-4;
   dQ, dK, dV: relative Frobenius error <= 1e-2.
+Each bar is applied per head (per query head for O and dQ, per kv head for
+dK and dV) and also per row: every row's error norm must stay within the
+same factor of the head's RMS row norm, so one wrong row (a broken diagonal
+or last tile) cannot hide inside a whole-tensor norm.  Rows whose reference
+is exactly zero (dQ of query 0) are covered by this form.
+The backward's row terms left in the workspace (D_i = rowsum(dO_i * O_i) at
+offset 0 and the base-2 LSE after it, both [B, Hq, S] fp32) are compared
+row by row as well.
 Also checked on the GPU outputs: causality (future keys / values do not
 change O or dQ of earlier rows: bit-identical), sum_j dK_j ~ 0 and
 sum_j dV_j = sum_i dO_i per kv head (pins the GQA reduction and the mask
@@ -18,7 +26,7 @@ import pytest
 
 import oracle
 from paper_2606_10415_amd.synth import attention_inputs
-from conftest import rel_f
+from conftest import rel_f, row_err
 
 pytestmark = pytest.mark.gpu
 
@@ -72,6 +80,7 @@ def run_attention(env, x, causal=True, fused=True, bwd=True):
                        dbase + 2 * (Hq + Hkv) * D, W2, W2, ws, ws_bytes, B, S, Hq, Hkv, D, scale,
                        int(causal))
         out["dQKV"] = dQKV
+        out["ws"] = ws
     torch.cuda.synchronize()
     res = {"O": out["O"].cpu().numpy().reshape(B, S, Hq, D), "LSE": out["LSE"].cpu().numpy()}
     if bwd:
@@ -79,46 +88,82 @@ def run_attention(env, x, causal=True, fused=True, bwd=True):
         res["dQ"] = d[:, :Hq * D].reshape(B, S, Hq, D)
         res["dK"] = d[:, Hq * D:(Hq + Hkv) * D].reshape(B, S, Hkv, D)
         res["dV"] = d[:, (Hq + Hkv) * D:].reshape(B, S, Hkv, D)
+        n = B * Hq * S
+        wsf = out["ws"].cpu().numpy()
+        off = (n * 4 + 255) // 256 * 256
+        res["ws_D"] = wsf[:n * 4].view(np.float32).reshape(B, Hq, S)
+        res["ws_LSE2"] = wsf[off:off + n * 4].view(np.float32).reshape(B, Hq, S)
+        res["dO"] = do
     return res
+
+
+def _per_head(err, name, got_rows, ref_rows):
+    """rel_F and the per-row bound of one head; keeps the worst of each in err."""
+    err[name] = max(err.get(name, 0.0), rel_f(got_rows, ref_rows))
+    err[name + "_row"] = max(err.get(name + "_row", 0.0), row_err(got_rows, ref_rows))
+
+
+def check_row_terms(got, lse_ref, delta_ref, heads):
+    """D and the base-2 LSE the backward leaves in its workspace, row by row.
+
+    D is compared with rowsum(dO * O) formed in float64 from the same fp16 dO
+    and the GPU's own fp16 O (per-op parity: fp32 accumulation of D products
+    allows ~D * 2^-24 per term), and with the oracle's definition
+    sum_j P_ij dP_ij (it differs by O's fp16 rounding: <= 5e-3 relative per head).
+    LSE2 must be LSE * log2(e) of the GPU's LSE to a few fp32 ulps and of the
+    oracle's LSE within the LSE bar times log2(e)."""
+    log2e = 1.0 / math.log(2.0)
+    o = got["O"].astype(np.float64)
+    do = got["dO"].astype(np.float64)
+    worst = {"D_perop": 0.0, "D_def": 0.0, "LSE2": 0.0}
+    for b, h in heads:
+        prod = do[b, :, h] * o[b, :, h]
+        d_perop = prod.sum(axis=1)
+        bound = 2e-5 * np.abs(prod).sum(axis=1) + 1e-6
+        e = np.abs(got["ws_D"][b, h] - d_perop)
+        assert np.all(e <= bound), (b, h, int(np.argmax(e - bound)), float(e.max()))
+        worst["D_perop"] = max(worst["D_perop"], float((e / bound).max()))
+        worst["D_def"] = max(worst["D_def"], rel_f(got["ws_D"][b, h], delta_ref[b, h]))
+        l2 = got["ws_LSE2"][b, h].astype(np.float64)
+        assert np.all(np.abs(l2 - got["LSE"][b, h].astype(np.float64) * log2e)
+                      <= 1e-6 * np.maximum(1.0, np.abs(l2))), (b, h)
+        worst["LSE2"] = max(worst["LSE2"], float(np.max(np.abs(l2 - lse_ref[b, h] * log2e))))
+    print("  row terms: " + ", ".join(f"{k} {v:.3e}" for k, v in worst.items()), flush=True)
+    assert worst["D_def"] <= 5e-3
+    assert worst["LSE2"] <= LSE_ABS_TOL * log2e
 
 
 def check_against_oracle(x, got, causal=True, heads=None, kv_heads=None):
     q, k, v, do = x["Q"], x["K"], x["V"], x["dO"]
-    D = q.shape[3]
+    B, S, Hq, D = q.shape
+    Hkv = k.shape[2]
+    g = Hq // Hkv
     scale = 1.0 / math.sqrt(D)
     o_ref, lse_ref = oracle.attn_fwd(q, k, v, scale, causal, heads=heads)
-    sel = [(slice(None), slice(None))] if heads is None else [(b, h) for b, h in heads]
-    err = {"O": 0.0, "LSE": 0.0}
-    for b, h in sel:
-        o_g = got["O"][b, :, h] if heads is not None else got["O"]
-        o_r = o_ref[b, :, h] if heads is not None else o_ref
-        l_g = got["LSE"][b, h] if heads is not None else got["LSE"]
-        l_r = lse_ref[b, h] if heads is not None else lse_ref
-        err["O"] = max(err["O"], rel_f(o_g, o_r))
-        err["LSE"] = max(err["LSE"], float(np.max(np.abs(l_g - l_r))))
+    qsel = [(b, h) for b in range(B) for h in range(Hq)] if heads is None else list(heads)
+    err = {"LSE": 0.0}
+    for b, h in qsel:
+        _per_head(err, "O", got["O"][b, :, h], o_ref[b, :, h])
+        err["LSE"] = max(err["LSE"], float(np.max(np.abs(got["LSE"][b, h] - lse_ref[b, h]))))
     if "dQ" in got:
         # per-op parity: the oracle backward gets the same fp16 inputs (its own P and row term)
-        dq, dk, dv, _ = oracle.attn_bwd(q, k, v, do, scale, causal, kv_heads=kv_heads)
-        g = q.shape[2] // k.shape[2]
-        kv_sel = [(slice(None), slice(None), slice(None))] if kv_heads is None else \
-            [(b, slice(kv * g, kv * g + g), kv) for b, kv in kv_heads]
-        for name in ("dQ", "dK", "dV"):
-            err[name] = 0.0
-        for b, hs, kv in kv_sel:
-            if kv_heads is None:
-                pairs = [("dQ", got["dQ"], dq), ("dK", got["dK"], dk), ("dV", got["dV"], dv)]
-            else:
-                pairs = [("dQ", got["dQ"][b, :, hs], dq[b, :, hs]),
-                         ("dK", got["dK"][b, :, kv], dk[b, :, kv]),
-                         ("dV", got["dV"][b, :, kv], dv[b, :, kv])]
-            for name, a_, r_ in pairs:
-                err[name] = max(err[name], rel_f(a_, r_))
+        dq, dk, dv, delta = oracle.attn_bwd(q, k, v, do, scale, causal, kv_heads=kv_heads)
+        kvsel = [(b, kv) for b in range(B) for kv in range(Hkv)] if kv_heads is None \
+            else list(kv_heads)
+        for b, kv in kvsel:
+            for h in range(kv * g, kv * g + g):
+                _per_head(err, "dQ", got["dQ"][b, :, h], dq[b, :, h])
+            _per_head(err, "dK", got["dK"][b, :, kv], dk[b, :, kv])
+            _per_head(err, "dV", got["dV"][b, :, kv], dv[b, :, kv])
+        check_row_terms(got, lse_ref, delta,
+                        [(b, h) for b, kv in kvsel for h in range(kv * g, kv * g + g)])
     print("  errors: " + ", ".join(f"{k_} {v_:.3e}" for k_, v_ in err.items()), flush=True)
-    assert err["O"] <= 5e-3
+    assert err["O"] <= 5e-3 and err["O_row"] <= 5e-3
     assert err["LSE"] <= LSE_ABS_TOL
     for name in ("dQ", "dK", "dV"):
         if name in err:
             assert err[name] <= 1e-2, name
+            assert err[name + "_row"] <= 1e-2, name + " (per row)"
 
 
 CASES = [
@@ -193,8 +238,9 @@ def test_attention_causality_and_invariants(env):
     ("llama2-7b", 1, 4096, 32, 32, 128, [(0, 0), (0, 31)]),
     ("qwen2.5-32b", 1, 4096, 40, 8, 128, [(0, 5)]),
     # 2 x 8 kv heads x 32 key tiles: the group's 8 query heads split in two
-    # dK/dV workgroups per key tile, partial sums added by the sum kernel
-    ("llama2-70b", 2, 4096, 64, 8, 128, [(1, 3)]),
+    # dK/dV workgroups per key tile, partial sums added by the sum kernel;
+    # both sequences of the micro-batch
+    ("llama2-70b", 2, 4096, 64, 8, 128, [(0, 3), (1, 3)]),
 ])
 def test_attention_full_size_sampled(env, name, B, S, Hq, Hkv, D, heads):
     """Full-size attention in the benchmark's launch configuration; whole

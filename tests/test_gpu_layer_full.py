@@ -7,11 +7,14 @@ of the layer is checked against the float64 oracle on outputs the oracle can
 compute one by one, taking that step's inputs from the GPU's own buffers:
 sampled rows of each activation / input-gradient product, sampled entries of
 each weight gradient (full-length dot products over the T tokens), and whole
-attention heads (forward O and LSE, backward dQ, dK, dV) for sampled heads of the
-last sequence of the micro-batch.
+attention heads (forward O and LSE, backward dQ, dK, dV) for sampled heads of
+every sequence of the micro-batch (with grouped queries, every query head of
+the sampled kv head for dQ).
 
 Bars: relative Frobenius error <= 5e-3 for GEMM outputs, SwiGLU outputs and
-attention O; <= 1e-2 for dQ, dK, dV; LSE absolute error <= 1e-4.
+attention O; <= 1e-2 for dQ, dK, dV; LSE absolute error <= 1e-4.  Attention
+heads also meet their bar per row (each row's error norm against the head's
+RMS row norm).
 """
 
 import numpy as np
@@ -19,7 +22,7 @@ import pytest
 
 import oracle
 from paper_2606_10415_amd.synth import WORKLOADS, layer_inputs
-from conftest import rel_f
+from conftest import rel_f, row_err
 
 pytestmark = pytest.mark.gpu
 
@@ -38,8 +41,7 @@ def test_full_size_layer_step_sampled(name, heads):
     torch.cuda.synchronize()
     c = lambda t: t.cpu().numpy()
     T, H, F, D = w.T, w.H, w.F, w.D
-    S, bi = w.S, w.B - 1                               # attention: the last sequence
-    seq = slice(bi * S, (bi + 1) * S)
+    S = w.S
     qd, kd = w.Hq * D, w.Hkv * D
     rng = np.random.default_rng(99)
     rows = np.unique(np.concatenate([rng.choice(T, 14, replace=False), [0, 1, T - 1]]))
@@ -47,6 +49,10 @@ def test_full_size_layer_step_sampled(name, heads):
     QKV, O, LSE, H1, GU, A, Y = (c(L.QKV), c(L.O), c(L.LSE), c(L.H1), c(L.GU), c(L.A), c(L.Y))
     dGU, dH1, dO, dQKV, dX = c(L.dGU), c(L.dH1), c(L.dO), c(L.dQKV), c(L.dX)
     err = {}
+
+    def attn(name, got, ref):                          # whole head: rel_F and per-row bound
+        err[name] = rel_f(got, ref)
+        err[name + "_row"] = row_err(got, ref)
 
     def ent(tA, tB, Am, Bm, out):                      # sampled weight-gradient entries
         r = rng.integers(0, out.shape[0], 48)
@@ -57,33 +63,39 @@ def test_full_size_layer_step_sampled(name, heads):
     err["QKV"] = rel_f(QKV[rows], oracle.gemm(0, 1, 1.0, X[rows], p["Wqkv"]))
     scale = 1.0 / np.sqrt(D)
     g = w.Hq // w.Hkv
-    for h in heads:
-        kv = h // g
-        q = QKV[seq, h * D:(h + 1) * D]
-        k = QKV[seq, qd + kv * D:qd + (kv + 1) * D]
-        v = QKV[seq, qd + kd + kv * D:qd + kd + (kv + 1) * D]
-        o, lse, _ = oracle.attn_head_fwd(q, k, v, scale, causal=True)
-        err[f"O[h{h}]"] = rel_f(O[seq, h * D:(h + 1) * D], o)
-        lse_err = float(np.max(np.abs(LSE[bi, h] - lse)))
-        assert lse_err <= 1e-4, (h, lse_err)
-        gr = oracle.attn_head_bwd(q, k, v, dO[seq, h * D:(h + 1) * D], scale, causal=True)
-        err[f"dQ[h{h}]"] = rel_f(dQKV[seq, h * D:(h + 1) * D], gr["dq"])
-        if g == 1:     # MHA: dK, dV of this kv head come from this query head alone
-            err[f"dK[h{h}]"] = rel_f(dQKV[seq, qd + kv * D:qd + (kv + 1) * D], gr["dk"])
-            err[f"dV[h{h}]"] = rel_f(dQKV[seq, qd + kd + kv * D:qd + kd + (kv + 1) * D], gr["dv"])
-    if g > 1:          # GQA: the kv head's gradient sums its g query heads
-        kv = heads[0] // g
-        k = QKV[seq, qd + kv * D:qd + (kv + 1) * D]
-        v = QKV[seq, qd + kd + kv * D:qd + kd + (kv + 1) * D]
-        dk = np.zeros((S, D))
-        dv = np.zeros((S, D))
-        for h in range(kv * g, (kv + 1) * g):
-            gr = oracle.attn_head_bwd(QKV[seq, h * D:(h + 1) * D], k, v, dO[seq, h * D:(h + 1) * D],
-                                      scale, causal=True)
-            dk += gr["dk"]
-            dv += gr["dv"]
-        err[f"dK[kv{kv}]"] = rel_f(dQKV[seq, qd + kv * D:qd + (kv + 1) * D], dk)
-        err[f"dV[kv{kv}]"] = rel_f(dQKV[seq, qd + kd + kv * D:qd + kd + (kv + 1) * D], dv)
+    for bi in range(w.B):                              # every sequence of the micro-batch
+        seq = slice(bi * S, (bi + 1) * S)
+
+        def head(base, i):
+            return QKV[seq, base + i * D:base + (i + 1) * D]
+
+        for h in heads:
+            kv = h // g
+            q, k, v = head(0, h), head(qd, kv), head(qd + kd, kv)
+            o, lse, _ = oracle.attn_head_fwd(q, k, v, scale, causal=True)
+            attn(f"O[b{bi}h{h}]", O[seq, h * D:(h + 1) * D], o)
+            lse_err = float(np.max(np.abs(LSE[bi, h] - lse)))
+            assert lse_err <= 1e-4, (bi, h, lse_err)
+            gr = oracle.attn_head_bwd(q, k, v, dO[seq, h * D:(h + 1) * D], scale, causal=True)
+            attn(f"dQ[b{bi}h{h}]", dQKV[seq, h * D:(h + 1) * D], gr["dq"])
+            if g == 1:     # MHA: dK, dV of this kv head come from this query head alone
+                attn(f"dK[b{bi}h{h}]", dQKV[seq, qd + kv * D:qd + (kv + 1) * D], gr["dk"])
+                attn(f"dV[b{bi}h{h}]", dQKV[seq, qd + kd + kv * D:qd + kd + (kv + 1) * D],
+                     gr["dv"])
+        if g > 1:          # GQA: the kv head's gradient sums its g query heads
+            kv = heads[0] // g
+            k, v = head(qd, kv), head(qd + kd, kv)
+            dk = np.zeros((S, D))
+            dv = np.zeros((S, D))
+            for h in range(kv * g, (kv + 1) * g):
+                gr = oracle.attn_head_bwd(head(0, h), k, v, dO[seq, h * D:(h + 1) * D], scale,
+                                          causal=True)
+                dk += gr["dk"]
+                dv += gr["dv"]
+                if h not in heads:
+                    attn(f"dQ[b{bi}h{h}]", dQKV[seq, h * D:(h + 1) * D], gr["dq"])
+            attn(f"dK[b{bi}kv{kv}]", dQKV[seq, qd + kv * D:qd + (kv + 1) * D], dk)
+            attn(f"dV[b{bi}kv{kv}]", dQKV[seq, qd + kd + kv * D:qd + kd + (kv + 1) * D], dv)
     err["H1"] = rel_f(H1[rows], oracle.gemm(0, 1, 1.0, O[rows], p["Wo"], 1.0, X[rows]))
     gu = oracle.gemm(0, 1, 1.0, H1[rows], p["Wgu"])
     err["GU"] = rel_f(GU[rows], gu)
