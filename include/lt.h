@@ -160,6 +160,30 @@ lt_status lt_gemm_f16_ws(int transA, int transB, int64_t M, int64_t N,
                          size_t workspace_bytes, lt_stream stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid hipMalloc): lt_gemm_f16_ws
+ * with its split-K workspace taken from a static device array of
+ * LT_GEMM_NOALLOC_SCRATCH_BYTES per GPU, held until the process ends, instead
+ * of a caller buffer.  Same product, same split and the same bits as
+ * lt_gemm_f16_ws with a sufficient workspace.  The call allocates nothing;
+ * its first call on a device looks up that device's array (once).  The
+ * current device must be the device of `stream` (else LT_ERR_INVALID_ARG).
+ * 64 MiB is what the largest split of any shape needs (a split covers at
+ * most 256 partial 256x256 FP32 tiles); a shape needing more
+ * (lt_gemm_f16_workspace_size) would be rejected with LT_ERR_WORKSPACE.  Every
+ * call on a GPU shares that GPU's array: calls that may overlap on one GPU
+ * (unordered streams) race and must not be issued.  Other errors as
+ * lt_gemm_f16_ws.
+ */
+#define LT_GEMM_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+lt_status lt_gemm_f16_noalloc(int transA, int transB, int64_t M, int64_t N,
+                              int64_t K, float alpha, const lt_half* A,
+                              int64_t lda, const lt_half* B, int64_t ldb,
+                              float beta, const lt_half* R, int64_t ldr,
+                              const lt_half* bias, lt_half* C, int64_t ldc,
+                              lt_stream stream);
+
+/*
  * Bias gradient of a linear layer: db[n] = sum over t < T of dY[t][n]
  * (dY row-major [T, N] with row stride lddy).  FP32 sums in a fixed order
  * (deterministic), one rounding to FP16.  The caller-owned workspace, of at

@@ -22,7 +22,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 SOURCES = ["lt_api.cpp", "plan.cpp", "gemm_f16.hip", "attn_fwd.hip", "attn_bwd.hip", "swiglu.hip", "norm_rope.hip",
-           "bias_grad.hip"]
+           "bias_grad.hip", "noalloc.hip"]
 
 COMMON_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

@@ -174,6 +174,15 @@ inline size_t bias_grad_ws_bytes(int64_t T, int64_t N) {
   return align256((size_t)bias_grad_blocks(T) * (size_t)N * sizeof(float));
 }
 
+// lt_api.cpp: the argument checks and dispatch behind the GEMM entry points
+// (also used by the allocation-free entry point), and the calling thread's
+// error message.
+lt_status gemm_checked(int transA, int transB, int64_t M, int64_t N, int64_t K, float alpha,
+                       const lt_half* A, int64_t lda, const lt_half* B, int64_t ldb, float beta,
+                       const lt_half* R, int64_t ldr, const lt_half* bias, lt_half* C, int64_t ldc,
+                       lt_stream stream, void* workspace, size_t ws_bytes);
+lt_status set_error(lt_status s, const char* msg);
+
 hipError_t gemm_f16_launch(const GemmArgs& a, hipStream_t s);
 hipError_t bias_grad_launch(const lt_half* dY, int64_t lddy, int64_t T, int64_t N, lt_half* db,
                             float* part, hipStream_t s);

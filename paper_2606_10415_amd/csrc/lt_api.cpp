@@ -114,6 +114,17 @@ static lt_status gemm_common(int transA, int transB, int64_t M, int64_t N, int64
   return from_hip(lt::gemm_f16_launch(g, reinterpret_cast<hipStream_t>(stream)), "gemm launch");
 }
 
+namespace lt {
+lt_status gemm_checked(int transA, int transB, int64_t M, int64_t N, int64_t K, float alpha,
+                       const lt_half* A, int64_t lda, const lt_half* B, int64_t ldb, float beta,
+                       const lt_half* R, int64_t ldr, const lt_half* bias, lt_half* C, int64_t ldc,
+                       lt_stream stream, void* workspace, size_t ws_bytes) {
+  return gemm_common(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, R, ldr, bias, C, ldc,
+                     stream, workspace, ws_bytes);
+}
+lt_status set_error(lt_status s, const char* msg) { return fail(s, "%s", msg); }
+}  // namespace lt
+
 extern "C" {
 
 const char* lt_status_string(lt_status s) {

@@ -94,6 +94,10 @@ _lib.lt_gemm_f16_workspace_size.argtypes = [_int, _int, _i64, _i64, _i64]
 _lib.lt_gemm_f16_ws.restype = _int
 _lib.lt_gemm_f16_ws.argtypes = [_int, _int, _i64, _i64, _i64, ctypes.c_float, _vp, _i64, _vp, _i64,
                                 ctypes.c_float, _vp, _i64, _vp, _vp, _i64, _vp, _sz, _vp]
+_lib.lt_gemm_f16_noalloc.restype = _int
+_lib.lt_gemm_f16_noalloc.argtypes = [_int, _int, _i64, _i64, _i64, ctypes.c_float, _vp, _i64, _vp,
+                                     _i64, ctypes.c_float, _vp, _i64, _vp, _vp, _i64, _vp]
+LT_GEMM_NOALLOC_SCRATCH_BYTES = 64 << 20
 _lib.lt_bias_grad_workspace_size.restype = ctypes.c_size_t
 _lib.lt_bias_grad_workspace_size.argtypes = [_i64, _i64]
 _lib.lt_bias_grad_f16.restype = _int
@@ -215,6 +219,14 @@ def lt_gemm_f16_ws(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, R, ldr,
                                _ptr(A), int(lda), _ptr(B), int(ldb), float(beta), _ptr(R), int(ldr),
                                _ptr(bias), _ptr(C), int(ldc), _ptr(workspace), int(ws_bytes),
                                _stream(stream)), "lt_gemm_f16_ws")
+
+
+def lt_gemm_f16_noalloc(transA, transB, M, N, K, alpha, A, lda, B, ldb, beta, R, ldr, bias, C, ldc,
+                        stream=None):
+    _check(_lib.lt_gemm_f16_noalloc(int(transA), int(transB), int(M), int(N), int(K), float(alpha),
+                                    _ptr(A), int(lda), _ptr(B), int(ldb), float(beta), _ptr(R),
+                                    int(ldr), _ptr(bias), _ptr(C), int(ldc), _stream(stream)),
+           "lt_gemm_f16_noalloc")
 
 
 def lt_bias_grad_workspace_size(T, N):
