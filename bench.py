@@ -199,7 +199,7 @@ def sweep():
         O = torch.empty(T, Hq * D, dtype=torch.float16, device="cuda")
         dQKV = torch.empty_like(QKV)
         LSE = torch.empty(B, Hq, S, dtype=torch.float32, device="cuda")
-        wsb = lt.lt_attn_bwd_workspace_size(B, S, Hq, Hkv, D)
+        wsb = lt.lt_attn_bwd_workspace_size(B, S, Hq, Hkv, D, 1)
         ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
         p, dp, sc = QKV.data_ptr(), dQKV.data_ptr(), 1.0 / math.sqrt(D)
         q, k, v = p, p + 2 * Hq * D, p + 2 * (Hq + Hkv) * D

@@ -227,34 +227,41 @@ lt_status lt_attn_fwd(const lt_half* Q, const lt_half* K, const lt_half* V,
                       lt_stream stream);
 
 /*
- * Bytes of device workspace lt_attn_bwd needs: the per-row term
- * D_i = rowsum(dO_i * O_i) [B, Hq, S] FP32 and the row LSE in base 2
- * [B, Hq, S] FP32, each 256-byte aligned.  The dK/dV pass takes 256-key
- * tiles, except for MHA (Hq = Hkv) when those give fewer than 512
- * workgroups over all batches and key/value heads: then 128-key tiles.
- * When the chosen tiles still give
- * fewer than 512 workgroups (few kv heads, short sequences) the workspace
- * also holds FP32 partial dK and dV sums [2][n][B, S, Hkv, D]: each key
- * tile's (query head, 64-query block) pairs are then split into n contiguous
- * shares, one workgroup each, and the partials are summed in a fixed order,
- * so results stay deterministic.  0 for invalid sizes.
+ * Bytes of device workspace lt_attn_bwd needs, each part 256-byte aligned,
+ * in this order:
+ *   D_i = rowsum(dO_i * O_i)              [B, Hq, S] FP32 (offset 0)
+ *   the row LSE in base 2                 [B, Hq, S] FP32
+ *   dS = P * (dP - D) in FP16, one 2 KiB block per (32-key group, 32-query
+ *   group) pair the mask keeps (n32 (n32 + 1) / 2 per (batch, query head)
+ *   under the causal mask, n32^2 without, n32 = ceil(S / 32)): written by the
+ *   dK/dV pass, read by the dQ pass;
+ *   FP32 partial dK and dV sums [2][n][B, S, Hkv, D] when the dK/dV work is
+ *   split into n > 1 shares.
+ * The dK/dV pass takes 256-key tiles, except for MHA (Hq = Hkv) when those
+ * give fewer than 512 workgroups over all batches and key/value heads: then
+ * 128-key tiles.  When the chosen tiles still give fewer than 512 workgroups
+ * (few kv heads, short sequences) each key tile's (query head, 64-query
+ * block) pairs are split into n contiguous shares, one workgroup each, and
+ * the partials are summed in a fixed order, so results stay deterministic.
+ * 0 for invalid sizes.
  */
-size_t lt_attn_bwd_workspace_size(int B, int S, int Hq, int Hkv, int D);
+size_t lt_attn_bwd_workspace_size(int B, int S, int Hq, int Hkv, int D, int causal);
 
 /*
  * Attention backward (Sec. 4.1, Algorithm 1: GP = GO V^T,
  * GS = SoftmaxBackward(P, GP), GV = P^T GO, GQ = GS K, GK = GS^T Q).
  * P is recomputed as exp(scale * q.k - LSE) from the forward's LSE instead of
  * being read back; SoftmaxBackward is GS_ij = P_ij (GP_ij - D_i) with
- * D_i = rowsum(dO_i * O_i).  dQ and dK carry the factor `scale`.
+ * D_i = rowsum(dO_i * O_i).  GS is kept in FP16 between the key-major pass
+ * (GV, GK) and the query-major GQ = GS K.  dQ and dK carry the factor `scale`.
  * dK and dV of a key/value head sum over its Hq/Hkv query heads.
  *
  *   Q, K, V, O, dO, LSE: as written by / passed to lt_attn_fwd (O and dO share
  *   o_row_stride).  dQ uses dq_row_stride, dK and dV use dkv_row_stride, so
  *   they may be column slices of one fused dQKV buffer.  dQ, dK, dV are
  *   overwritten.  `workspace` is a device buffer of at least
- *   lt_attn_bwd_workspace_size(...) bytes, 256-byte aligned, owned by the
- *   caller; its contents on entry are ignored.
+ *   lt_attn_bwd_workspace_size(B, S, Hq, Hkv, D, causal) bytes, 256-byte
+ *   aligned, owned by the caller; its contents on entry are ignored.
  *   Errors: as lt_attn_fwd (every row stride, dq_row_stride and
  *   dkv_row_stride included, must be < 2^22 elements), plus LT_ERR_WORKSPACE
  *   if workspace is NULL or ws_bytes is too small.
@@ -267,6 +274,49 @@ lt_status lt_attn_bwd(const lt_half* Q, const lt_half* K, const lt_half* V,
                       int64_t dkv_row_stride, void* workspace, size_t ws_bytes,
                       int B, int S, int Hq, int Hkv, int D, float scale,
                       int causal, lt_stream stream);
+
+/*
+ * Saved-P attention (Algorithm 1 as the paper states it: the backward loads
+ * the probability tiles P_ij the forward produced instead of recomputing
+ * them).  An alternative to lt_attn_bwd's recomputed P that trades HBM
+ * traffic and residency for MFMA work.
+ *
+ * lt_attn_p_size: bytes of the P buffer, one 2 KiB FP16 block per
+ *   (32-key group, 32-query group) pair the mask keeps (n32 (n32 + 1) / 2 per
+ *   (batch, query head) under the causal mask, n32^2 without,
+ *   n32 = ceil(S / 32)); 0 for invalid sizes.  0.54 GB at LLaMA-2-7B's 32
+ *   heads and S = 4096.
+ * lt_attn_fwd_p: lt_attn_fwd, then P = exp(scale q.k - LSE) of those blocks
+ *   into the caller's buffer P (p_bytes >= lt_attn_p_size, 16-byte aligned);
+ *   masked entries are exactly 0.  P stays valid for the matching
+ *   lt_attn_bwd_p.  Errors: as lt_attn_fwd; LT_ERR_WORKSPACE if p_bytes is
+ *   too small.
+ * lt_attn_bwd_p: the backward of lt_attn_bwd with P read from that buffer
+ *   (written by lt_attn_fwd_p for the same Q, K, shapes, scale and causal):
+ *   GV = P^T GO and GK = GS^T Q in a key-major pass whose GP = GO V^T is the
+ *   only product it forms, and GQ = GS K in a query-major pass that forms S
+ *   and GP itself (and D_i = rowsum(dO_i * O_i), run first).  The workspace
+ *   (lt_attn_bwd_p_workspace_size bytes, 256-byte aligned) holds D and the
+ *   base-2 LSE [B, Hq, S] FP32 and, when the dK/dV work is split into
+ *   shares, FP32 partial dK, dV as for lt_attn_bwd.  Errors: as lt_attn_bwd,
+ *   plus LT_ERR_INVALID_ARG for a NULL or too small P.
+ */
+size_t lt_attn_p_size(int B, int S, int Hq, int causal);
+lt_status lt_attn_fwd_p(const lt_half* Q, const lt_half* K, const lt_half* V,
+                        int64_t q_row_stride, int64_t kv_row_stride, lt_half* O,
+                        int64_t o_row_stride, float* LSE, lt_half* P,
+                        size_t p_bytes, int B, int S, int Hq, int Hkv, int D,
+                        float scale, int causal, lt_stream stream);
+size_t lt_attn_bwd_p_workspace_size(int B, int S, int Hq, int Hkv, int D);
+lt_status lt_attn_bwd_p(const lt_half* Q, const lt_half* K, const lt_half* V,
+                        int64_t q_row_stride, int64_t kv_row_stride,
+                        const lt_half* O, const lt_half* dO,
+                        int64_t o_row_stride, const float* LSE,
+                        const lt_half* P, size_t p_bytes, lt_half* dQ,
+                        lt_half* dK, lt_half* dV, int64_t dq_row_stride,
+                        int64_t dkv_row_stride, void* workspace,
+                        size_t ws_bytes, int B, int S, int Hq, int Hkv, int D,
+                        float scale, int causal, lt_stream stream);
 
 /*
  * SwiGLU gate joining the FFN gate/up projection and the down projection.

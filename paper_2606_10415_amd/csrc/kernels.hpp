@@ -87,9 +87,22 @@ struct AttnBwdArgs {
   int64_t dq_stride, dkv_stride;
   float* delta;   // workspace: [B, Hq, S]  rowsum(dO * O)
   float* lse2;    // workspace: [B, Hq, S]  LSE * log2(e)
+  lt_half* ds;    // workspace: dS blocks [B, Hq, n_blocks(S, causal)][64 lanes][16] FP16
   float* part;    // workspace: [2][nsplit][B, S, Hkv, D] partial dK, dV (nsplit > 1 only)
   int nsplit;     // shares of each key tile's work in the dK/dV pass
   int ktile;      // keys per dK/dV workgroup (256 or 128)
+  const lt_half* psaved = nullptr;   // saved P blocks (saved-P backward only)
+};
+
+// Saved P (written after the forward, read by the saved-P backward): the
+// dS block layout (attn_bwd_ds_blocks) holding P instead of dS.
+struct AttnSavePArgs {
+  AttnShape sh;
+  const lt_half* Q;
+  const lt_half* K;
+  int64_t q_stride, kv_stride;
+  const float* LSE;
+  lt_half* P;
 };
 
 // Workspace layout of the attention backward (offsets in bytes).
@@ -98,6 +111,20 @@ inline size_t attn_bwd_delta_bytes(int B, int S, int Hq) {
   return align256((size_t)B * Hq * S * sizeof(float));
 }
 inline size_t attn_bwd_lse2_bytes(int B, int S, int Hq) { return attn_bwd_delta_bytes(B, S, Hq); }
+// dS of every (32-key group, 32-query group) pair the mask keeps, as the
+// dK/dV pass holds it in registers: one 2 KiB block per pair, lane l's 16
+// FP16 values (key l % 32; queries 8 (j / 4) + 4 (l / 32) + j % 4, j = 0..15)
+// at bytes 32 l.  Blocks of a head are query-major: under the causal mask
+// query group qg holds key groups 0..qg, at qg (qg + 1) / 2 + kg; otherwise
+// qg * n32 + kg.  The dQ pass streams a query group's blocks in order.
+constexpr int kDsBlockBytes = 2048;
+inline int64_t attn_bwd_ds_blocks(int S, int causal) {   // per (batch, query head)
+  const int64_t n32 = ((int64_t)S + 31) / 32;
+  return causal ? n32 * (n32 + 1) / 2 : n32 * n32;
+}
+inline size_t attn_bwd_ds_bytes(int B, int S, int Hq, int causal) {
+  return align256((size_t)B * Hq * (size_t)attn_bwd_ds_blocks(S, causal) * kDsBlockBytes);
+}
 // The dK/dV pass runs one workgroup per (key tile, batch, kv head, share),
 // one workgroup per CU.  Key tiles hold 256 keys (8 waves of 32), except
 // for MHA (Hq = Hkv) when those give fewer than 512 workgroups: then 128
@@ -188,6 +215,8 @@ hipError_t bias_grad_launch(const lt_half* dY, int64_t lddy, int64_t T, int64_t 
                             float* part, hipStream_t s);
 hipError_t attn_fwd_launch(const AttnFwdArgs& a, hipStream_t s);
 hipError_t attn_bwd_launch(const AttnBwdArgs& a, hipStream_t s);
+hipError_t attn_save_p_launch(const AttnSavePArgs& a, hipStream_t s);
+hipError_t attn_bwd_p_launch(const AttnBwdArgs& a, hipStream_t s);
 hipError_t rmsnorm_fwd_launch(const lt_half* X, int64_t ldx, const lt_half* W, lt_half* Y,
                               int64_t ldy, float* RSTD, int64_t T, int64_t H, float eps,
                               hipStream_t s);

@@ -70,6 +70,30 @@ lt_status check_attn_common(const void* Q, const void* K, const void* V, int64_t
   return LT_OK;
 }
 
+lt_status check_attn_bwd(const void* Q, const void* K, const void* V, int64_t q_row_stride,
+                         int64_t kv_row_stride, const void* O, const void* dO, int64_t o_row_stride,
+                         const float* LSE, const void* dQ, const void* dK, const void* dV,
+                         int64_t dq_row_stride, int64_t dkv_row_stride, int B, int S, int Hq,
+                         int Hkv, int D, float scale, int causal) {
+  lt_status st = check_attn_common(Q, K, V, q_row_stride, kv_row_stride, B, S, Hq, Hkv, D, scale,
+                                   causal);
+  if (st != LT_OK) return st;
+  if (!O || !dO || !LSE || !dQ || !dK || !dV)
+    return fail(LT_ERR_INVALID_ARG, "NULL O/dO/LSE/dQ/dK/dV pointer");
+  if (o_row_stride < (int64_t)Hq * D || dq_row_stride < (int64_t)Hq * D ||
+      dkv_row_stride < (int64_t)Hkv * D)
+    return fail(LT_ERR_INVALID_ARG, "o/dq/dkv row stride smaller than the row length");
+  if ((o_row_stride | dq_row_stride | dkv_row_stride) & 7)
+    return fail(LT_ERR_UNSUPPORTED, "row strides must be multiples of 8 elements");
+  if (o_row_stride >= kMaxAttnStride || dq_row_stride >= kMaxAttnStride ||
+      dkv_row_stride >= kMaxAttnStride)
+    return fail(LT_ERR_UNSUPPORTED, "o/dq/dkv row strides must be < 2^22 elements");
+  if (!aligned16(O) || !aligned16(dO) || !aligned16(dQ) || !aligned16(dK) || !aligned16(dV))
+    return fail(LT_ERR_UNSUPPORTED, "O/dO/dQ/dK/dV must be 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(LSE) & 3u) return fail(LT_ERR_UNSUPPORTED, "LSE must be 4-byte aligned");
+  return LT_OK;
+}
+
 }  // namespace
 
 static lt_status gemm_common(int transA, int transB, int64_t M, int64_t N, int64_t K, float alpha,
@@ -223,11 +247,12 @@ lt_status lt_attn_fwd(const lt_half* Q, const lt_half* K, const lt_half* V, int6
   return from_hip(lt::attn_fwd_launch(a, reinterpret_cast<hipStream_t>(stream)), "attn_fwd launch");
 }
 
-size_t lt_attn_bwd_workspace_size(int B, int S, int Hq, int Hkv, int D) {
-  if (B < 1 || S < 1 || Hq < 1 || Hkv < 1 || D < 1 || Hq % Hkv) return 0;
+size_t lt_attn_bwd_workspace_size(int B, int S, int Hq, int Hkv, int D, int causal) {
+  if (B < 1 || S < 1 || Hq < 1 || Hkv < 1 || D < 1 || Hq % Hkv || (causal != 0 && causal != 1))
+    return 0;
   if (too_many_rows(B, S, Hq) || (D != 64 && D != 128)) return 0;   // lt_attn_bwd rejects these
   return lt::attn_bwd_delta_bytes(B, S, Hq) + lt::attn_bwd_lse2_bytes(B, S, Hq) +
-         lt::attn_bwd_part_bytes(B, S, Hq, Hkv, D);
+         lt::attn_bwd_ds_bytes(B, S, Hq, causal) + lt::attn_bwd_part_bytes(B, S, Hq, Hkv, D);
 }
 
 lt_status lt_attn_bwd(const lt_half* Q, const lt_half* K, const lt_half* V, int64_t q_row_stride,
@@ -236,41 +261,102 @@ lt_status lt_attn_bwd(const lt_half* Q, const lt_half* K, const lt_half* V, int6
                       int64_t dq_row_stride, int64_t dkv_row_stride, void* workspace,
                       size_t ws_bytes, int B, int S, int Hq, int Hkv, int D, float scale,
                       int causal, lt_stream stream) {
-  lt_status st = check_attn_common(Q, K, V, q_row_stride, kv_row_stride, B, S, Hq, Hkv, D, scale,
-                                   causal);
+  lt_status st = check_attn_bwd(Q, K, V, q_row_stride, kv_row_stride, O, dO, o_row_stride, LSE, dQ,
+                                dK, dV, dq_row_stride, dkv_row_stride, B, S, Hq, Hkv, D, scale,
+                                causal);
   if (st != LT_OK) return st;
-  if (!O || !dO || !LSE || !dQ || !dK || !dV)
-    return fail(LT_ERR_INVALID_ARG, "NULL O/dO/LSE/dQ/dK/dV pointer");
-  if (o_row_stride < (int64_t)Hq * D || dq_row_stride < (int64_t)Hq * D ||
-      dkv_row_stride < (int64_t)Hkv * D)
-    return fail(LT_ERR_INVALID_ARG, "o/dq/dkv row stride smaller than the row length");
-  if ((o_row_stride | dq_row_stride | dkv_row_stride) & 7)
-    return fail(LT_ERR_UNSUPPORTED, "row strides must be multiples of 8 elements");
-  if (o_row_stride >= kMaxAttnStride || dq_row_stride >= kMaxAttnStride ||
-      dkv_row_stride >= kMaxAttnStride)
-    return fail(LT_ERR_UNSUPPORTED, "o/dq/dkv row strides must be < 2^22 elements");
-  if (!aligned16(O) || !aligned16(dO) || !aligned16(dQ) || !aligned16(dK) || !aligned16(dV))
-    return fail(LT_ERR_UNSUPPORTED, "O/dO/dQ/dK/dV must be 16-byte aligned");
-  if (reinterpret_cast<uintptr_t>(LSE) & 3u) return fail(LT_ERR_UNSUPPORTED, "LSE must be 4-byte aligned");
-  const size_t need = lt_attn_bwd_workspace_size(B, S, Hq, Hkv, D);
+  const size_t need = lt_attn_bwd_workspace_size(B, S, Hq, Hkv, D, causal);
   if (!workspace || ws_bytes < need)
     return fail(LT_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
                 workspace ? ws_bytes : (size_t)0);
   if (reinterpret_cast<uintptr_t>(workspace) & 255u)
     return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned");
   char* ws = static_cast<char*>(workspace);
+  const size_t off_lse2 = lt::attn_bwd_delta_bytes(B, S, Hq);
+  const size_t off_ds = off_lse2 + lt::attn_bwd_lse2_bytes(B, S, Hq);
+  const size_t off_part = off_ds + lt::attn_bwd_ds_bytes(B, S, Hq, causal);
   lt::AttnBwdArgs a{{B, S, Hq, Hkv, D, scale, causal},
                     Q, K, V, q_row_stride, kv_row_stride, O, dO, o_row_stride, LSE, dQ, dK, dV,
                     dq_row_stride, dkv_row_stride,
                     reinterpret_cast<float*>(ws),
-                    reinterpret_cast<float*>(ws + lt::attn_bwd_delta_bytes(B, S, Hq)),
-                    reinterpret_cast<float*>(ws + lt::attn_bwd_delta_bytes(B, S, Hq) +
-                                             lt::attn_bwd_lse2_bytes(B, S, Hq)),
+                    reinterpret_cast<float*>(ws + off_lse2),
+                    reinterpret_cast<lt_half*>(ws + off_ds),
+                    reinterpret_cast<float*>(ws + off_part),
                     0, 0};
   const lt::DkdvPlan plan = lt::attn_bwd_dkdv_plan(B, S, Hq, Hkv);
   a.nsplit = plan.nsplit;
   a.ktile = plan.ktile;
   return from_hip(lt::attn_bwd_launch(a, reinterpret_cast<hipStream_t>(stream)), "attn_bwd launch");
+}
+
+size_t lt_attn_p_size(int B, int S, int Hq, int causal) {
+  if (B < 1 || S < 1 || Hq < 1 || (causal != 0 && causal != 1)) return 0;
+  if (too_many_rows(B, S, Hq)) return 0;
+  return lt::attn_bwd_ds_bytes(B, S, Hq, causal);
+}
+
+lt_status lt_attn_fwd_p(const lt_half* Q, const lt_half* K, const lt_half* V,
+                        int64_t q_row_stride, int64_t kv_row_stride, lt_half* O,
+                        int64_t o_row_stride, float* LSE, lt_half* P, size_t p_bytes, int B, int S,
+                        int Hq, int Hkv, int D, float scale, int causal, lt_stream stream) {
+  if (!P) return fail(LT_ERR_INVALID_ARG, "NULL P");
+  lt_status st = lt_attn_fwd(Q, K, V, q_row_stride, kv_row_stride, O, o_row_stride, LSE, B, S, Hq,
+                             Hkv, D, scale, causal, stream);
+  if (st != LT_OK) return st;
+  // lt_attn_fwd validated the shape; the P blocks follow it on the same stream
+  const size_t need = lt_attn_p_size(B, S, Hq, causal);
+  if (p_bytes < need)
+    return fail(LT_ERR_WORKSPACE, "P buffer of %zu bytes needed, %zu given", need, p_bytes);
+  if (!aligned16(P)) return fail(LT_ERR_UNSUPPORTED, "P must be 16-byte aligned");
+  lt::AttnSavePArgs a{{B, S, Hq, Hkv, D, scale, causal}, Q, K, q_row_stride, kv_row_stride, LSE, P};
+  return from_hip(lt::attn_save_p_launch(a, reinterpret_cast<hipStream_t>(stream)),
+                  "attn_save_p launch");
+}
+
+size_t lt_attn_bwd_p_workspace_size(int B, int S, int Hq, int Hkv, int D) {
+  if (B < 1 || S < 1 || Hq < 1 || Hkv < 1 || D < 1 || Hq % Hkv) return 0;
+  if (too_many_rows(B, S, Hq) || (D != 64 && D != 128)) return 0;
+  return lt::attn_bwd_delta_bytes(B, S, Hq) + lt::attn_bwd_lse2_bytes(B, S, Hq) +
+         lt::attn_bwd_part_bytes(B, S, Hq, Hkv, D);
+}
+
+lt_status lt_attn_bwd_p(const lt_half* Q, const lt_half* K, const lt_half* V, int64_t q_row_stride,
+                        int64_t kv_row_stride, const lt_half* O, const lt_half* dO,
+                        int64_t o_row_stride, const float* LSE, const lt_half* P, size_t p_bytes,
+                        lt_half* dQ, lt_half* dK, lt_half* dV, int64_t dq_row_stride,
+                        int64_t dkv_row_stride, void* workspace, size_t ws_bytes, int B, int S,
+                        int Hq, int Hkv, int D, float scale, int causal, lt_stream stream) {
+  lt_status st = check_attn_bwd(Q, K, V, q_row_stride, kv_row_stride, O, dO, o_row_stride, LSE, dQ,
+                                dK, dV, dq_row_stride, dkv_row_stride, B, S, Hq, Hkv, D, scale,
+                                causal);
+  if (st != LT_OK) return st;
+  if (!P) return fail(LT_ERR_INVALID_ARG, "NULL P");
+  const size_t pneed = lt_attn_p_size(B, S, Hq, causal);
+  if (p_bytes < pneed)
+    return fail(LT_ERR_INVALID_ARG, "P buffer of %zu bytes expected, %zu given", pneed, p_bytes);
+  if (!aligned16(P)) return fail(LT_ERR_UNSUPPORTED, "P must be 16-byte aligned");
+  const size_t need = lt_attn_bwd_p_workspace_size(B, S, Hq, Hkv, D);
+  if (!workspace || ws_bytes < need)
+    return fail(LT_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                workspace ? ws_bytes : (size_t)0);
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(LT_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  char* ws = static_cast<char*>(workspace);
+  const size_t off_lse2 = lt::attn_bwd_delta_bytes(B, S, Hq);
+  const size_t off_part = off_lse2 + lt::attn_bwd_lse2_bytes(B, S, Hq);
+  lt::AttnBwdArgs a{{B, S, Hq, Hkv, D, scale, causal},
+                    Q, K, V, q_row_stride, kv_row_stride, O, dO, o_row_stride, LSE, dQ, dK, dV,
+                    dq_row_stride, dkv_row_stride,
+                    reinterpret_cast<float*>(ws),
+                    reinterpret_cast<float*>(ws + off_lse2),
+                    nullptr,
+                    reinterpret_cast<float*>(ws + off_part),
+                    0, 0, P};
+  const lt::DkdvPlan plan = lt::attn_bwd_dkdv_plan(B, S, Hq, Hkv);
+  a.nsplit = plan.nsplit;
+  a.ktile = plan.ktile;
+  return from_hip(lt::attn_bwd_p_launch(a, reinterpret_cast<hipStream_t>(stream)),
+                  "attn_bwd_p launch");
 }
 
 lt_status lt_gemm_gu_swiglu_f16(const lt_half* X, int64_t ldx, const lt_half* Wgu, int64_t ldw,

@@ -91,7 +91,7 @@ class DecoderLayer:
             self.dO = e(T, self.hd)
             self.dQKV = e(T, self.qkv)
             self.dX = e(T, sh.H)
-            self.ws_bytes = lt.lt_attn_bwd_workspace_size(sh.B, sh.S, sh.Hq, sh.Hkv, sh.D)
+            self.ws_bytes = lt.lt_attn_bwd_workspace_size(sh.B, sh.S, sh.Hq, sh.Hkv, sh.D, 1)
             self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.dev)
             # split-K workspace of the plain GEMM calls (one at a time on the
             # stream); the fused SwiGLU GEMMs take none

@@ -78,10 +78,20 @@ _lib.lt_attn_fwd.restype = _int
 _lib.lt_attn_fwd.argtypes = [_vp, _vp, _vp, _i64, _i64, _vp, _i64, _vp, _int, _int, _int, _int, _int,
                              _f32, _int, _vp]
 _lib.lt_attn_bwd_workspace_size.restype = _sz
-_lib.lt_attn_bwd_workspace_size.argtypes = [_int, _int, _int, _int, _int]
+_lib.lt_attn_bwd_workspace_size.argtypes = [_int, _int, _int, _int, _int, _int]
 _lib.lt_attn_bwd.restype = _int
 _lib.lt_attn_bwd.argtypes = [_vp, _vp, _vp, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp, _i64, _i64,
                              _vp, _sz, _int, _int, _int, _int, _int, _f32, _int, _vp]
+_lib.lt_attn_p_size.restype = _sz
+_lib.lt_attn_p_size.argtypes = [_int, _int, _int, _int]
+_lib.lt_attn_fwd_p.restype = _int
+_lib.lt_attn_fwd_p.argtypes = [_vp, _vp, _vp, _i64, _i64, _vp, _i64, _vp, _vp, _sz, _int, _int, _int,
+                               _int, _int, _f32, _int, _vp]
+_lib.lt_attn_bwd_p_workspace_size.restype = _sz
+_lib.lt_attn_bwd_p_workspace_size.argtypes = [_int, _int, _int, _int, _int]
+_lib.lt_attn_bwd_p.restype = _int
+_lib.lt_attn_bwd_p.argtypes = [_vp, _vp, _vp, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _sz, _vp, _vp, _vp,
+                               _i64, _i64, _vp, _sz, _int, _int, _int, _int, _int, _f32, _int, _vp]
 _lib.lt_swiglu_fwd.restype = _int
 _lib.lt_swiglu_fwd.argtypes = [_vp, _vp, _i64, _i64, _vp]
 _lib.lt_swiglu_bwd.restype = _int
@@ -178,8 +188,9 @@ def lt_attn_fwd(Q, K, V, q_row_stride, kv_row_stride, O, o_row_stride, LSE, B, S
                             float(scale), int(causal), _stream(stream)), "lt_attn_fwd")
 
 
-def lt_attn_bwd_workspace_size(B, S, Hq, Hkv, D):
-    return int(_lib.lt_attn_bwd_workspace_size(int(B), int(S), int(Hq), int(Hkv), int(D)))
+def lt_attn_bwd_workspace_size(B, S, Hq, Hkv, D, causal):
+    return int(_lib.lt_attn_bwd_workspace_size(int(B), int(S), int(Hq), int(Hkv), int(D),
+                                               int(causal)))
 
 
 def lt_attn_bwd(Q, K, V, q_row_stride, kv_row_stride, O, dO, o_row_stride, LSE, dQ, dK, dV,
@@ -190,6 +201,33 @@ def lt_attn_bwd(Q, K, V, q_row_stride, kv_row_stride, O, dO, o_row_stride, LSE, 
                             int(dq_row_stride), int(dkv_row_stride), _ptr(workspace), int(ws_bytes),
                             int(B), int(S), int(Hq), int(Hkv), int(D), float(scale), int(causal),
                             _stream(stream)), "lt_attn_bwd")
+
+
+def lt_attn_p_size(B, S, Hq, causal):
+    return int(_lib.lt_attn_p_size(int(B), int(S), int(Hq), int(causal)))
+
+
+def lt_attn_fwd_p(Q, K, V, q_row_stride, kv_row_stride, O, o_row_stride, LSE, P, p_bytes, B, S, Hq,
+                  Hkv, D, scale, causal, stream=None):
+    _check(_lib.lt_attn_fwd_p(_ptr(Q), _ptr(K), _ptr(V), int(q_row_stride), int(kv_row_stride),
+                              _ptr(O), int(o_row_stride), _ptr(LSE), _ptr(P), int(p_bytes), int(B),
+                              int(S), int(Hq), int(Hkv), int(D), float(scale), int(causal),
+                              _stream(stream)), "lt_attn_fwd_p")
+
+
+def lt_attn_bwd_p_workspace_size(B, S, Hq, Hkv, D):
+    return int(_lib.lt_attn_bwd_p_workspace_size(int(B), int(S), int(Hq), int(Hkv), int(D)))
+
+
+def lt_attn_bwd_p(Q, K, V, q_row_stride, kv_row_stride, O, dO, o_row_stride, LSE, P, p_bytes, dQ, dK,
+                  dV, dq_row_stride, dkv_row_stride, workspace, ws_bytes, B, S, Hq, Hkv, D, scale,
+                  causal, stream=None):
+    _check(_lib.lt_attn_bwd_p(_ptr(Q), _ptr(K), _ptr(V), int(q_row_stride), int(kv_row_stride),
+                              _ptr(O), _ptr(dO), int(o_row_stride), _ptr(LSE), _ptr(P), int(p_bytes),
+                              _ptr(dQ), _ptr(dK), _ptr(dV), int(dq_row_stride),
+                              int(dkv_row_stride), _ptr(workspace), int(ws_bytes), int(B), int(S),
+                              int(Hq), int(Hkv), int(D), float(scale), int(causal),
+                              _stream(stream)), "lt_attn_bwd_p")
 
 
 def lt_swiglu_fwd(GU, A, T, F, stream=None):

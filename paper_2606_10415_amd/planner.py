@@ -127,7 +127,7 @@ class ModelProfile:
         half = T * (self.F + 2 * self.F + self.H + self.Hq * self.D + self.qkv_cols + 2 * self.H
                     + (2 * self.H if self.norm else 0))
         from . import lt
-        attn_ws = lt.lt_attn_bwd_workspace_size(b, S, self.Hq, self.Hkv, self.D)
+        attn_ws = lt.lt_attn_bwd_workspace_size(b, S, self.Hq, self.Hkv, self.D, 1)
         return 2 * half + attn_ws + self.gemm_workspace(b, S)
 
 

@@ -69,8 +69,22 @@ hipError_t attn_bwd_launch(const AttnBwdArgs& a, hipStream_t) {
   const AttnShape& s = a.sh;
   ws_inside(a.delta, attn_bwd_delta_bytes(s.B, s.S, s.Hq), "D");
   ws_inside(a.lse2, attn_bwd_lse2_bytes(s.B, s.S, s.Hq), "LSE2");
+  ws_inside(a.ds, attn_bwd_ds_bytes(s.B, s.S, s.Hq, s.causal), "dS blocks");
   if (a.nsplit > 1) ws_inside(a.part, attn_bwd_part_bytes(s.B, s.S, s.Hq, s.Hkv, s.D), "dK/dV partials");
   CHECK(a.nsplit >= 1 && (a.ktile == 128 || a.ktile == 256), "dK/dV plan %d %d", a.nsplit, a.ktile);
+  return hipErrorNoDevice;
+}
+hipError_t attn_save_p_launch(const AttnSavePArgs&, hipStream_t) {
+  ++g_launches;
+  return hipErrorNoDevice;
+}
+hipError_t attn_bwd_p_launch(const AttnBwdArgs& a, hipStream_t) {
+  ++g_launches;
+  const AttnShape& s = a.sh;
+  ws_inside(a.delta, attn_bwd_delta_bytes(s.B, s.S, s.Hq), "D");
+  ws_inside(a.lse2, attn_bwd_lse2_bytes(s.B, s.S, s.Hq), "LSE2");
+  if (a.nsplit > 1) ws_inside(a.part, attn_bwd_part_bytes(s.B, s.S, s.Hq, s.Hkv, s.D), "dK/dV partials");
+  CHECK(a.psaved != nullptr && a.ds == nullptr, "saved-P arguments");
   return hipErrorNoDevice;
 }
 hipError_t rmsnorm_fwd_launch(const lt_half*, int64_t, const lt_half*, lt_half*, int64_t, float*,
@@ -172,7 +186,7 @@ static void documented_cases() {
          LT_ERR_UNSUPPORTED, "attn_fwd stride >= 2^22");
   expect(lt_attn_fwd(H, H, H, 384, 384, H, 128, F32, 1, 16, 2, 1, 64, 0.125f, 1, nullptr),
          LT_ERR_HIP, "attn_fwd valid");
-  const size_t aws = lt_attn_bwd_workspace_size(2, 100, 8, 2, 128);
+  const size_t aws = lt_attn_bwd_workspace_size(2, 100, 8, 2, 128, 1);
   CHECK(aws > 0 && aws % 256 == 0, "attn_bwd workspace size %zu", aws);
   set_ws(WS, aws);
   expect(lt_attn_bwd(H, H, H, 1536, 1536, H, H, 1024, F32, H, H, H, 1536, 1536, WS, aws - 1, 2,
@@ -185,8 +199,22 @@ static void documented_cases() {
                      2, 128, 0.09f, 1, nullptr),
          LT_ERR_HIP, "attn_bwd valid");
   set_ws(nullptr, 0);
-  CHECK(lt_attn_bwd_workspace_size(0, 100, 8, 2, 128) == 0, "attn ws B = 0");
-  CHECK(lt_attn_bwd_workspace_size(1, 100, 8, 3, 128) == 0, "attn ws Hq %% Hkv");
+  const size_t pb = lt_attn_p_size(2, 100, 8, 1);
+  CHECK(pb == 2 * 8 * 10 * 2048, "saved-P size %zu", pb);
+  expect(lt_attn_fwd_p(H, H, H, 1536, 1536, H, 1024, F32, H, pb - 1, 2, 100, 8, 2, 128, 0.09f, 1,
+                       nullptr),
+         LT_ERR_HIP, "attn_fwd_p: the forward launch fails first without a device");
+  const size_t pws = lt_attn_bwd_p_workspace_size(2, 100, 8, 2, 128);
+  set_ws(WS, pws);
+  expect(lt_attn_bwd_p(H, H, H, 1536, 1536, H, H, 1024, F32, H, pb - 1, H, H, H, 1536, 1536, WS, pws,
+                       2, 100, 8, 2, 128, 0.09f, 1, nullptr),
+         LT_ERR_INVALID_ARG, "attn_bwd_p short P");
+  expect(lt_attn_bwd_p(H, H, H, 1536, 1536, H, H, 1024, F32, H, pb, H, H, H, 1536, 1536, WS, pws,
+                       2, 100, 8, 2, 128, 0.09f, 1, nullptr),
+         LT_ERR_HIP, "attn_bwd_p valid");
+  set_ws(nullptr, 0);
+  CHECK(lt_attn_bwd_workspace_size(0, 100, 8, 2, 128, 1) == 0, "attn ws B = 0");
+  CHECK(lt_attn_bwd_workspace_size(1, 100, 8, 3, 128, 1) == 0, "attn ws Hq %% Hkv");
 
   // ---- SwiGLU, norms, rotary, bias ----
   expect(lt_swiglu_fwd(H, H, 4, 12, nullptr), LT_ERR_UNSUPPORTED, "swiglu F % 8");
@@ -236,13 +264,23 @@ static void fuzz(unsigned seed, int rounds) {
     lt_gemm_swiglu_bwd_f16(ptr(H), pick64(), ptr(H), pick64(), ptr(H), pick64(), ptr(H), pick64(),
                            M, N, K, nullptr);
     const int B = pick32(), S = pick32(), Hq = pick32(), Hkv = pick32(), D = rng() % 2 ? 128 : pick32();
-    const size_t aws = lt_attn_bwd_workspace_size(B, S, Hq, Hkv, D);
+    const int causal = (int)(rng() % 3);
+    const size_t aws = lt_attn_bwd_workspace_size(B, S, Hq, Hkv, D, causal);
     set_ws(WS, aws);
     lt_attn_fwd(ptr(H), ptr(H), ptr(H), pick64(), pick64(), ptr(H), pick64(), ptr(F32), B, S, Hq, Hkv,
                 D, rng() % 5 ? 0.088f : -1.f, (int)(rng() % 3), nullptr);
     lt_attn_bwd(ptr(H), ptr(H), ptr(H), pick64(), pick64(), ptr(H), ptr(H), pick64(), ptr(F32),
                 ptr(H), ptr(H), ptr(H), pick64(), pick64(), rng() % 4 ? WS : nullptr, aws, B, S, Hq,
-                Hkv, D, 0.088f, (int)(rng() % 3), nullptr);
+                Hkv, D, 0.088f, causal, nullptr);
+    const size_t pb = lt_attn_p_size(B, S, Hq, causal);
+    lt_attn_fwd_p(ptr(H), ptr(H), ptr(H), pick64(), pick64(), ptr(H), pick64(), ptr(F32), ptr(H),
+                  rng() % 2 ? pb : pb / 2, B, S, Hq, Hkv, D, 0.088f, causal, nullptr);
+    const size_t pws = lt_attn_bwd_p_workspace_size(B, S, Hq, Hkv, D);
+    set_ws(WS, pws);
+    lt_attn_bwd_p(ptr(H), ptr(H), ptr(H), pick64(), pick64(), ptr(H), ptr(H), pick64(), ptr(F32),
+                  ptr(H), rng() % 2 ? pb : 0, ptr(H), ptr(H), ptr(H), pick64(), pick64(),
+                  rng() % 4 ? WS : nullptr, pws, B, S, Hq, Hkv, D, 0.088f, causal, nullptr);
+    set_ws(nullptr, 0);
     const int64_t T = pick64(), Hd = pick64();
     const size_t rws = lt_rmsnorm_bwd_workspace_size(T, Hd);
     set_ws(WS, rws);

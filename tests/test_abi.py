@@ -17,9 +17,12 @@ def test_every_declared_symbol_is_exported():
             "lt_rmsnorm_bwd", "lt_rmsnorm_bwd_workspace_size", "lt_rope_table",
             "lt_rope_f16", "lt_gemm_gu_swiglu_f16", "lt_gemm_swiglu_bwd_f16", "lt_gemm_f16_bias",
             "lt_bias_grad_workspace_size", "lt_bias_grad_f16", "lt_gemm_f16_workspace_size",
-            "lt_gemm_f16_ws"} <= set(names)
+            "lt_gemm_f16_ws", "lt_gemm_f16_noalloc"} <= set(names)
     for n in names:
         assert hasattr(lt._lib, n), f"{n} declared in lt.h but not exported"
+    with open(lt.HEADER) as f:
+        assert "#define LT_GEMM_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)" in f.read()
+    assert lt.LT_GEMM_NOALLOC_SCRATCH_BYTES == 64 << 20
 
 
 def test_status_strings():
@@ -105,37 +108,56 @@ def _align256(x):
     return (x + 255) // 256 * 256
 
 
+def _ds_bytes(B, S, Hq, causal):
+    n32 = (S + 31) // 32
+    blocks = n32 * (n32 + 1) // 2 if causal else n32 * n32
+    return _align256(B * Hq * blocks * 2048)
+
+
 def test_attn_bwd_workspace():
-    # D and the base-2 LSE, [B, Hq, S] fp32 each, 256-byte aligned, plus fp32 partial
+    # D and the base-2 LSE, [B, Hq, S] fp32 each, then the fp16 dS blocks (2 KiB per
+    # 32-key x 32-query pair the mask keeps), each 256-byte aligned, plus fp32 partial
     # dK, dV [2][n][B, S, Hkv, D] when a key tile's (query head, query block) pairs are
     # split n ways.  Key tiles hold 256 keys, or 128 for MHA when 256-key tiles give fewer
     # than 512 workgroups (tiles x B x Hkv); with the chosen tiles, fewer than 512
     # workgroups split n ways: the
     # smallest divisor of Hq/Hkv reaching 512 workgroups, else min(max(Hq/Hkv,
     # ceil(256 / workgroups)), 16, the last key tile's pairs).
+    def rows(B, S, Hq):
+        return 2 * _align256(4 * B * Hq * S)
     # MHA, S = 100: 16 workgroups, 2 query blocks in the only key tile -> n = 2
-    assert lt.lt_attn_bwd_workspace_size(2, 100, 8, 8, 128) == \
-        2 * _align256(4 * 2 * 8 * 100) + _align256(2 * 2 * 2 * 100 * 8 * 128 * 4)
+    assert lt.lt_attn_bwd_workspace_size(2, 100, 8, 8, 128, 1) == \
+        rows(2, 100, 8) + _ds_bytes(2, 100, 8, 1) + _align256(2 * 2 * 2 * 100 * 8 * 128 * 4)
+    # non-causal: every (key group, query group) pair
+    assert lt.lt_attn_bwd_workspace_size(2, 100, 8, 8, 128, 0) == \
+        rows(2, 100, 8) + _ds_bytes(2, 100, 8, 0) + _align256(2 * 2 * 2 * 100 * 8 * 128 * 4)
+    assert _ds_bytes(1, 100, 1, 0) == 16 * 2048 and _ds_bytes(1, 100, 1, 1) == 10 * 2048
     # GQA 4:1, S = 100: 4 workgroups; max(4, 64) capped at 16, then at 4 heads x 2 blocks -> 8
-    ws = lt.lt_attn_bwd_workspace_size(2, 100, 8, 2, 128)
-    assert ws == 2 * _align256(4 * 2 * 8 * 100) + _align256(2 * 8 * 2 * 100 * 2 * 128 * 4)
+    ws = lt.lt_attn_bwd_workspace_size(2, 100, 8, 2, 128, 1)
+    assert ws == rows(2, 100, 8) + _ds_bytes(2, 100, 8, 1) + \
+        _align256(2 * 8 * 2 * 100 * 2 * 128 * 4)
     assert ws % 256 == 0
     # MHA, S = 1024, 32 heads: 128-key tiles, 256 workgroups -> n = 1, no partials
-    assert lt.lt_attn_bwd_workspace_size(1, 1024, 32, 32, 128) == 2 * _align256(4 * 32 * 1024)
+    assert lt.lt_attn_bwd_workspace_size(1, 1024, 32, 32, 128, 1) == \
+        rows(1, 1024, 32) + _ds_bytes(1, 1024, 32, 1)
     # MHA, S = 512: 128 workgroups of 128 keys; the last tile has 2 query blocks -> n = 2
-    assert lt.lt_attn_bwd_workspace_size(1, 512, 32, 32, 128) == \
-        2 * _align256(4 * 32 * 512) + _align256(2 * 2 * 512 * 32 * 128 * 4)
+    assert lt.lt_attn_bwd_workspace_size(1, 512, 32, 32, 128, 1) == \
+        rows(1, 512, 32) + _ds_bytes(1, 512, 32, 1) + _align256(2 * 2 * 512 * 32 * 128 * 4)
     # GQA 5:1, S = 2048: 64 workgroups of 256 keys, no divisor reaches 512 -> max(4, 5)
-    assert lt.lt_attn_bwd_workspace_size(1, 2048, 40, 8, 128) == \
-        2 * _align256(4 * 40 * 2048) + _align256(2 * 5 * 2048 * 8 * 128 * 4)
+    assert lt.lt_attn_bwd_workspace_size(1, 2048, 40, 8, 128, 1) == \
+        rows(1, 2048, 40) + _ds_bytes(1, 2048, 40, 1) + _align256(2 * 5 * 2048 * 8 * 128 * 4)
     # enough kv heads x key tiles (512 or more workgroups): no split, no partials
-    assert lt.lt_attn_bwd_workspace_size(1, 4096, 128, 32, 128) == 2 * _align256(4 * 128 * 4096)
-    assert lt.lt_attn_bwd_workspace_size(1, 4096, 32, 32, 128) == 2 * _align256(4 * 32 * 4096)
+    assert lt.lt_attn_bwd_workspace_size(1, 4096, 128, 32, 128, 1) == \
+        rows(1, 4096, 128) + _ds_bytes(1, 4096, 128, 1)
+    # LLaMA-2-7B heads: 32 x 8256 blocks of 2 KiB = 541 MB of dS
+    assert lt.lt_attn_bwd_workspace_size(1, 4096, 32, 32, 128, 1) == \
+        rows(1, 4096, 32) + 32 * 8256 * 2048
     # GQA 5:1 (Qwen2.5-32B heads), S = 4096: 128 workgroups of 256 keys, divisor 5 -> 640
-    assert lt.lt_attn_bwd_workspace_size(1, 4096, 40, 8, 128) == \
-        2 * _align256(4 * 40 * 4096) + _align256(2 * 5 * 4096 * 8 * 128 * 4)
-    assert lt.lt_attn_bwd_workspace_size(0, 100, 8, 2, 128) == 0
-    assert lt.lt_attn_bwd_workspace_size(1, 100, 8, 3, 128) == 0
+    assert lt.lt_attn_bwd_workspace_size(1, 4096, 40, 8, 128, 1) == \
+        rows(1, 4096, 40) + _ds_bytes(1, 4096, 40, 1) + _align256(2 * 5 * 4096 * 8 * 128 * 4)
+    assert lt.lt_attn_bwd_workspace_size(1, 100, 8, 2, 128, 2) == 0
+    assert lt.lt_attn_bwd_workspace_size(0, 100, 8, 2, 128, 1) == 0
+    assert lt.lt_attn_bwd_workspace_size(1, 100, 8, 3, 128, 1) == 0
     args = [FAKE, FAKE, FAKE, 1536, 1536, FAKE, FAKE, 1024, FAKE, FAKE, FAKE, FAKE, 1536, 1536]
     st = lt._lib.lt_attn_bwd(*args, FAKE, ws - 1, 2, 100, 8, 2, 128, 0.09, 1, None)
     assert st == lt.LT_ERR_WORKSPACE

@@ -45,9 +45,11 @@ def env():
     return torch, lt
 
 
-def run_attention(env, x, causal=True, fused=True, bwd=True):
+def run_attention(env, x, causal=True, fused=True, bwd=True, saved_p=False):
     """Run fwd (+bwd) on the GPU.  Q/K/V live in one fused [B*S, (Hq+2Hkv)D] buffer
-    (as the layer lays them out) when ``fused``; else in separate dense buffers."""
+    (as the layer lays them out) when ``fused``; else in separate dense buffers.
+    ``saved_p``: the forward also writes P (lt_attn_fwd_p) and the backward reads
+    it (lt_attn_bwd_p) instead of recomputing it."""
     torch, lt = env
     q, k, v, do = x["Q"], x["K"], x["V"], x["dO"]
     B, S, Hq, D = q.shape
@@ -69,22 +71,37 @@ def run_attention(env, x, causal=True, fused=True, bwd=True):
         qs, kvs = Hq * D, Hkv * D
     O = torch.empty(T, Hq * D, dtype=torch.float16, device="cuda")
     LSE = torch.empty(B, Hq, S, dtype=torch.float32, device="cuda")
-    lt.lt_attn_fwd(Qp, Kp, Vp, qs, kvs, O, Hq * D, LSE, B, S, Hq, Hkv, D, scale, int(causal))
+    if saved_p:
+        p_bytes = lt.lt_attn_p_size(B, S, Hq, int(causal))
+        P = torch.full((p_bytes // 2,), float("nan"), dtype=torch.float16, device="cuda")
+        lt.lt_attn_fwd_p(Qp, Kp, Vp, qs, kvs, O, Hq * D, LSE, P, p_bytes, B, S, Hq, Hkv, D, scale,
+                         int(causal))
+    else:
+        lt.lt_attn_fwd(Qp, Kp, Vp, qs, kvs, O, Hq * D, LSE, B, S, Hq, Hkv, D, scale, int(causal))
     out = {"O": O, "LSE": LSE}
     if bwd:
         dO = torch.from_numpy(do.reshape(T, Hq * D)).cuda()
         W2 = (Hq + 2 * Hkv) * D
         dQKV = torch.full((T, W2), float("nan"), dtype=torch.float16, device="cuda")
         dbase = dQKV.data_ptr()
-        ws_bytes = lt.lt_attn_bwd_workspace_size(B, S, Hq, Hkv, D)
-        ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
-        lt.lt_attn_bwd(Qp, Kp, Vp, qs, kvs, O, dO, Hq * D, LSE, dbase, dbase + 2 * Hq * D,
-                       dbase + 2 * (Hq + Hkv) * D, W2, W2, ws, ws_bytes, B, S, Hq, Hkv, D, scale,
-                       int(causal))
+        if saved_p:
+            ws_bytes = lt.lt_attn_bwd_p_workspace_size(B, S, Hq, Hkv, D)
+            ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+            lt.lt_attn_bwd_p(Qp, Kp, Vp, qs, kvs, O, dO, Hq * D, LSE, P, p_bytes, dbase,
+                             dbase + 2 * Hq * D, dbase + 2 * (Hq + Hkv) * D, W2, W2, ws, ws_bytes,
+                             B, S, Hq, Hkv, D, scale, int(causal))
+        else:
+            ws_bytes = lt.lt_attn_bwd_workspace_size(B, S, Hq, Hkv, D, int(causal))
+            ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+            lt.lt_attn_bwd(Qp, Kp, Vp, qs, kvs, O, dO, Hq * D, LSE, dbase, dbase + 2 * Hq * D,
+                           dbase + 2 * (Hq + Hkv) * D, W2, W2, ws, ws_bytes, B, S, Hq, Hkv, D,
+                           scale, int(causal))
         out["dQKV"] = dQKV
         out["ws"] = ws
     torch.cuda.synchronize()
     res = {"O": out["O"].cpu().numpy().reshape(B, S, Hq, D), "LSE": out["LSE"].cpu().numpy()}
+    if saved_p:
+        res["P"] = P.cpu().numpy()
     if bwd:
         d = out["dQKV"].cpu().numpy()
         res["dQ"] = d[:, :Hq * D].reshape(B, S, Hq, D)
@@ -217,6 +234,56 @@ def test_attention_parity(env, B, S, Hq, Hkv, D, causal):
     check_against_oracle(x, got, causal)
 
 
+def p_block(pbuf, B, S, Hq, b, h, qg, kg, causal):
+    """The stored [32 keys x 32 queries] P block of (b, h, query group qg, key group
+    kg) as a [query, key] matrix.  Block layout (lt.h): 2 KiB per block,
+    query-major (causal: qg (qg + 1) / 2 + kg), lane l = key l % 32 holding 16
+    values; value j is query 8 (j / 4) + 4 (l / 32) + j % 4."""
+    n32 = (S + 31) // 32
+    nblk = n32 * (n32 + 1) // 2 if causal else n32 * n32
+    blk = qg * (qg + 1) // 2 + kg if causal else qg * n32 + kg
+    base = ((b * Hq + h) * nblk + blk) * 1024               # in fp16 elements
+    lanes = pbuf[base:base + 1024].reshape(64, 16).astype(np.float64)
+    out = np.zeros((32, 32))
+    for l in range(64):
+        for j in range(16):
+            out[8 * (j // 4) + 4 * (l // 32) + j % 4, l % 32] = lanes[l, j]
+    return out
+
+
+@pytest.mark.parametrize("B,S,Hq,Hkv,D,causal", CASES)
+def test_attention_saved_p_parity(env, B, S, Hq, Hkv, D, causal):
+    """The saved-P pair (lt_attn_fwd_p, lt_attn_bwd_p) against the oracle, with the
+    same bars; the stored P blocks themselves against the oracle's P (each entry
+    within its fp16 rounding, masked entries exactly 0)."""
+    print(f"saved-P attention B={B} S={S} Hq={Hq} Hkv={Hkv} D={D} causal={causal}", flush=True)
+    x = attention_inputs(B, S, Hq, Hkv, D, seed_base=20000 + S)
+    got = run_attention(env, x, causal, saved_p=True)
+    check_against_oracle(x, got, causal)
+    rng = np.random.default_rng(S)
+    n32 = (S + 31) // 32
+    g = Hq // Hkv
+    worst = 0.0
+    for _ in range(6):
+        b, h = int(rng.integers(B)), int(rng.integers(Hq))
+        qg = int(rng.integers(n32))
+        kg = int(rng.integers(qg + 1)) if causal else int(rng.integers(n32))
+        _, _, pref = oracle.attn_head_fwd(x["Q"][b, :, h], x["K"][b, :, h // g], x["V"][b, :, h // g],
+                                          1.0 / math.sqrt(D), causal)
+        ref = np.zeros((32, 32))
+        q0, k0 = qg * 32, kg * 32
+        sub = pref[q0:q0 + 32, k0:k0 + 32]
+        ref[:sub.shape[0], :sub.shape[1]] = sub               # rows / keys past S stay 0
+        blk = p_block(got["P"], B, S, Hq, b, h, qg, kg, causal)
+        assert np.all(blk[ref == 0] == 0), (b, h, qg, kg)
+        err = np.abs(blk - ref)
+        # one fp16 rounding (2^-11 relative, 2^-25 absolute among subnormals) of an fp32
+        # value whose own error (score sums, exp2) is ~1e-6 relative
+        assert np.all(err <= (2.0 ** -11 + 1e-5) * ref + 2.0 ** -24), (b, h, qg, kg, float(err.max()))
+        worst = max(worst, float(err.max()))
+    print(f"  stored P blocks: max abs error {worst:.2e}", flush=True)
+
+
 def test_attention_large_scores(env):
     """Q, K scaled x8 (score std ~ 64 before scaling): exercises max subtraction."""
     x = attention_inputs(1, 160, 2, 1, 64, seed_base=21000, qk_std=8.0)
@@ -250,6 +317,20 @@ def test_attention_causality_and_invariants(env):
         dv_sum = a["dV"][0, :, kv].astype(np.float64).sum(axis=0)
         ref = do[0, :, kv * g:(kv + 1) * g].sum(axis=(0, 1))
         assert rel_f(dv_sum, ref) <= 1e-2
+
+
+@pytest.mark.parametrize("name,B,S,Hq,Hkv,D,heads", [
+    ("llama2-7b", 1, 4096, 32, 32, 128, [(0, 7)]),
+    ("qwen2.5-32b", 1, 4096, 40, 8, 128, [(0, 2)]),
+])
+def test_attention_saved_p_full_size_sampled(env, name, B, S, Hq, Hkv, D, heads):
+    """The saved-P pair at full size in the benchmark's launch configuration."""
+    print(f"saved-P attention full-size {name}", flush=True)
+    x = attention_inputs(B, S, Hq, Hkv, D, seed_base=24000)
+    got = run_attention(env, x, True, saved_p=True)
+    g = Hq // Hkv
+    q_heads = [(b, h) for b, kv in heads for h in range(kv * g, kv * g + g)]
+    check_against_oracle(x, got, True, heads=q_heads, kv_heads=list(heads))
 
 
 @pytest.mark.parametrize("name,B,S,Hq,Hkv,D,heads", [
