@@ -183,10 +183,10 @@ struct RmsBwdArgs {
   float* part;           // workspace
   int64_t T, H;
 };
-constexpr int kRmsBwdWaves = 8;
-inline int rmsnorm_bwd_blocks(int64_t T) {   // about one row per wave, at most 512 workgroups
+constexpr int kRmsBwdWaves = 4;
+inline int rmsnorm_bwd_blocks(int64_t T) {   // about one row per wave, at most 1024 workgroups
   const int64_t b = T / kRmsBwdWaves + (T % kRmsBwdWaves != 0);   // no overflow at any T
-  return (int)(b < 512 ? (b < 1 ? 1 : b) : 512);
+  return (int)(b < 1024 ? (b < 1 ? 1 : b) : 1024);
 }
 inline size_t rmsnorm_bwd_ws_bytes(int64_t T, int64_t H) {
   return align256((size_t)rmsnorm_bwd_blocks(T) * H * sizeof(float));

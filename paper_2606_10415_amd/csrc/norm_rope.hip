@@ -6,7 +6,7 @@
 //     l, l + 64, ... of the row (coalesced), the sum of squares is a wave
 //     shuffle reduction; writes y = w * x * r (one rounding) and r.
 //       r = (mean_j x_j^2 + eps)^(-1/2)
-//   * rmsnorm_bwd: the same row layout, 8 waves per workgroup, about one row
+//   * rmsnorm_bwd: the same row layout, 4 waves per workgroup, about one row
 //     per wave; per row
 //       dx = r * w * g - r^3 * x / H * sum_j g_j w_j x_j   (+ residual R)
 //     with g and x held in registers between the row dot product and dx
@@ -108,15 +108,18 @@ rmsnorm_bwd_kernel(const lt_half* __restrict__ dY, int64_t lddy, const lt_half* 
     const float r = RSTD[row];
     const lt_half* gp = dY + row * lddy;
     const lt_half* xp = X + row * ldx;
-    half8 gk[ONEPASS ? MAXK : 1], xk[ONEPASS ? MAXK : 1];
+    half8 gk[ONEPASS ? MAXK : 1], xk[ONEPASS ? MAXK : 1], rk[ONEPASS ? MAXK : 1];
     float dot = 0.f;
 #pragma unroll
     for (int k = 0; k < MAXK; ++k) {
       const int c = lane + 64 * k;
-      half8 gv = as_half8(u32x4{0, 0, 0, 0}), xv = gv;
+      half8 gv = as_half8(u32x4{0, 0, 0, 0}), xv = gv, rv = gv;
       if (c < nch) {
         gv = as_half8(ld16(gp + c * 8));
         xv = as_half8(ld16(xp + c * 8));
+        // rows up to 4096 columns: the residual row is loaded with g and x
+        // (one memory latency per row); wider rows load it later, for registers
+        if (ONEPASS && MAXK <= 8 && R) rv = as_half8(ld16(R + row * ldr + c * 8));
         const half8 wv = as_half8(ld16(W + c * 8));
 #pragma unroll
         for (int e = 0; e < 8; ++e) dot += (float)gv[e] * (float)wv[e] * (float)xv[e];
@@ -124,6 +127,7 @@ rmsnorm_bwd_kernel(const lt_half* __restrict__ dY, int64_t lddy, const lt_half* 
       if constexpr (ONEPASS) {
         gk[k] = gv;
         xk[k] = xv;
+        rk[k] = rv;
       }
     }
     dot = wave_sum(dot);
@@ -136,7 +140,8 @@ rmsnorm_bwd_kernel(const lt_half* __restrict__ dY, int64_t lddy, const lt_half* 
         const half8 xv = ONEPASS ? xk[k] : as_half8(ld16(xp + c * 8));
         const half8 wv = as_half8(ld16(W + c * 8));
         half8 rv = as_half8(u32x4{0, 0, 0, 0});
-        if (R) rv = as_half8(ld16(R + row * ldr + c * 8));
+        if (ONEPASS && MAXK <= 8) rv = rk[k];
+        else if (R) rv = as_half8(ld16(R + row * ldr + c * 8));
         half8 o;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
@@ -157,12 +162,15 @@ rmsnorm_bwd_kernel(const lt_half* __restrict__ dY, int64_t lddy, const lt_half* 
 #pragma unroll
     for (int e = 0; e < 8; ++e) red[wave][lane * 8 + e] = dw[k][e];
     __syncthreads();
-    const int t = threadIdx.x;                      // column 512 k + t
-    if (64 * k + t / 8 < nch) {
-      float sum = 0.f;
+    // columns 512 k + t, t = thread, thread + 64 kBwdWaves, ...
 #pragma unroll
-      for (int v = 0; v < kBwdWaves; ++v) sum += red[v][t];
-      dst[512 * k + t] = sum;
+    for (int t = threadIdx.x; t < 512; t += 64 * kBwdWaves) {
+      if (64 * k + t / 8 < nch) {
+        float sum = 0.f;
+#pragma unroll
+        for (int v = 0; v < kBwdWaves; ++v) sum += red[v][t];
+        dst[512 * k + t] = sum;
+      }
     }
     __syncthreads();
   }
@@ -170,7 +178,8 @@ rmsnorm_bwd_kernel(const lt_half* __restrict__ dY, int64_t lddy, const lt_half* 
 
 // dW[j] = sum over the partial rows; FP16 result.  Workgroup = 16 waves over
 // 64 columns (lane = column, coalesced): wave v sums partial rows v, v + 16,
-// ... in order, then wave 0 adds the 16 wave sums in order (deterministic).
+// ... in order (eight loads in flight at a time), then wave 0 adds the 16
+// wave sums in order (deterministic).
 constexpr int kSumWaves = 16;
 
 __global__ void __launch_bounds__(64 * kSumWaves)
@@ -180,8 +189,19 @@ rmsnorm_dw_sum_kernel(const float* __restrict__ part, int nparts, int H, lt_half
   const int wave = threadIdx.x >> 6;
   const int j = blockIdx.x * 64 + lane;
   float s = 0.f;
-  if (j < H)
-    for (int t = wave; t < nparts; t += kSumWaves) s += part[(int64_t)t * H + j];
+  if (j < H) {
+    // eight partial rows loaded together, added in row order
+    for (int t = wave; t < nparts; t += 8 * kSumWaves) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int tu = t + u * kSumWaves;
+        v[u] = tu < nparts ? part[(int64_t)tu * H + j] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+  }
   red[wave][lane] = s;
   __syncthreads();
   if (wave == 0 && j < H) {
