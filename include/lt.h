@@ -29,9 +29,10 @@
  *   - Float16 outputs are rounded once, round-to-nearest-even, from the
  *     FP32 accumulator; FP16 subnormals are kept.
  *   - Fast-path alignment: every half pointer must be 16-byte aligned and
- *     every leading dimension / row stride a multiple of 8 elements; the
- *     GEMM also needs M, N, K to be multiples of 8.  Otherwise the call
- *     returns LT_ERR_UNSUPPORTED (it never computes a wrong result).
+ *     every leading dimension / row stride a multiple of 8 elements.
+ *     Otherwise the call returns LT_ERR_UNSUPPORTED (it never computes a
+ *     wrong result).  The plain GEMMs take any M, N, K; the fused entry
+ *     points state their own size rules.
  */
 #ifndef LT_H_
 #define LT_H_
@@ -82,10 +83,16 @@ int lt_version(void);
  *     forward  Y  = X  W^T  -> (transA, transB) = (0, 1)
  *     dgrad    dX = dY W    -> (0, 0)
  *     wgrad    dW = dY^T X  -> (1, 0)   (beta = 1 accumulates micro-batches)
+ *   Tails: any M, N, K.  Operand rows are read in whole 8-element (16-byte)
+ *   chunks, so each stored row of A, B (and R below) must be readable up to
+ *   its length rounded up to a multiple of 8 -- within its leading
+ *   dimension, so true of any buffer that spans whole leading dimensions;
+ *   elements past the row length never reach a stored result.  C is written
+ *   only inside its M x N part.
  *   Errors: LT_ERR_INVALID_ARG for NULL A/B/C (C may be NULL only if M or N
  *   is 0), negative sizes, trans not 0/1, ld smaller than the row length;
- *   LT_ERR_UNSUPPORTED for M, N, K or an ld not a multiple of 8, a pointer
- *   not 16-byte aligned, or lda / ldb >= 2^22 elements.
+ *   LT_ERR_UNSUPPORTED for an ld not a multiple of 8, a pointer not 16-byte
+ *   aligned, M, N or K > 2^30, or lda / ldb >= 2^22 elements.
  */
 lt_status lt_gemm_f16(int transA, int transB, int64_t M, int64_t N, int64_t K,
                       float alpha, const lt_half* A, int64_t lda,
@@ -142,7 +149,8 @@ lt_status lt_gemm_f16_bias(int transA, int transB, int64_t M, int64_t N,
  *   keeps at least 2048 of K per share.  Their FP32 partial sums go to the
  *   workspace and are added in a fixed order (deterministic) before the
  *   single rounding of C.  The result can differ from lt_gemm_f16_res in the
- *   last bits of those tiles (another FP32 summation order).
+ *   last bits of those tiles (another FP32 summation order).  There is no
+ *   split (workspace size 0) when N or K is not a multiple of 8.
  *   workspace: device memory owned by the caller, 16-byte aligned (else
  *   LT_ERR_UNSUPPORTED), of at least lt_gemm_f16_workspace_size(...) bytes
  *   (else LT_ERR_WORKSPACE); its contents on entry do not matter and it is

@@ -163,6 +163,28 @@ struct Operand {
     }
   }
 
+  // K % 8 != 0 (K-contiguous tiles only; the k-major layout loads whole
+  // k-rows, so its rows past K are already zero): the chunk of each row that
+  // straddles K was loaded whole and holds the row's next elements in memory
+  // (padding up to the leading dimension) past K.  Threads t < R of the
+  // workgroup zero elements kvalid % 8 .. 7 of row t's chunk kvalid / 8 in
+  // the LDS tile.  Called between the barrier after which the slice is
+  // resident and a barrier before its first fragment read.
+  __device__ __forceinline__ void zero_k_tail(char* lds, int kvalid, int t) const {
+    static_assert(KC, "k-major tiles need no fix-up");
+    if (t < 0 || t >= R) return;
+    const int e0 = kvalid & 7;
+    char* q = lds + t * (CPR * 16) + (((kvalid >> 3) ^ swz(t)) << 4);
+    u32x4 v = *reinterpret_cast<const u32x4*>(q);
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      // 16-bit elements 2w and 2w + 1 of the chunk
+      const uint32_t keep = (2 * w < e0 ? 0x0000ffffu : 0u) | (2 * w + 1 < e0 ? 0xffff0000u : 0u);
+      v[w] &= keep;
+    }
+    *reinterpret_cast<u32x4*>(q) = v;
+  }
+
   // MFMA operand (16x16x32): rows rb..rb+15 (lane row = lane % 16),
   // reduction indices kk*32 + 8*(lane/16) + 0..7.
   __device__ __forceinline__ half8 frag(const char* lds, int rb, int kk, int lane) const {
@@ -206,7 +228,8 @@ __device__ __forceinline__ void wait_slices(int n) {
 
 __device__ __forceinline__ float sigmoid_f(float x) { return 1.f / (1.f + __expf(-x)); }
 
-template <int BM, int BN, int WGM, int WGN, int BK, int NS, bool TA, bool TB, int EPI>
+template <int BM, int BN, int WGM, int WGN, int BK, int NS, bool TA, bool TB, int EPI,
+          bool RK = false>
 __global__ void __launch_bounds__(WGM * WGN * kWave)
 gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
                 const lt_half* __restrict__ A, int64_t lda,
@@ -293,6 +316,24 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
     oa.load(st, (int64_t)kt * BK, kvalid(kt), wave, lane);
     ob.load(st + OA::BYTES, (int64_t)kt * BK, kvalid(kt), wave, lane);
   };
+  // RK (ragged K, not a multiple of 8; plain epilogue only): the last
+  // slice's K-contiguous tiles are cleared past K, between two barriers.  A
+  // separate instantiation, so that no branch sits at the slice barrier of
+  // the other kernels (their first MFMAs after it are scheduled across it).
+  static_assert(!RK || EPI == 0, "ragged K: plain epilogue");
+  constexpr bool KFIX = RK && (!TA || TB);
+  static_assert(!KFIX || (TA ? 0 : BM) + (TB ? BN : 0) <= NT, "one thread per tile row");
+  auto fix_k_tail = [&](int kt) {
+    if constexpr (KFIX) {
+      char* st = stage_of(kt);
+      const int kv = kvalid(kt);
+      if constexpr (!TA) oa.zero_k_tail(st, kv, tid);
+      if constexpr (TB) ob.zero_k_tail(st + OA::BYTES, kv, TA ? tid : tid - BM);
+      __syncthreads();
+    }
+  };
+  constexpr bool ragged_k = KFIX;
+
   // Fragments: A in place (each re-read right after its last use), B
   // double-buffered (used by every A row of a step).
   half8 fa[TM], fb[2][TN];
@@ -303,6 +344,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
     if (s < nk) issue(s);
   wait_slices<PER_SLICE, NS - 1>(min(NS - 1, nk - 1));
   __syncthreads();
+  if (ragged_k && nk == 1) fix_k_tail(0);
 
   // One MFMA step on (fa, fb[S]).  With LD, the fragments of the next step
   // (32-wide k-step kk of stage st) are read meanwhile: after the MFMAs of A
@@ -384,6 +426,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
     // slices after kt+1 that are already issued may stay in flight
     wait_slices<PER_SLICE, NS - 2>(min(kt + NS - 1, nk - 1) - (kt + 1));
     __syncthreads();
+    if (ragged_k && kt + 2 == nk) fix_k_tail(kt + 1);
     // (after the last slice these reads of a stale stage are unused; reading
     // unconditionally keeps one copy of the fragments live across the loop)
     step(C1{}, YES{}, stage_of(kt + 1), 0, [&](auto part) {
@@ -471,7 +514,14 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int64_t n = nb + j * 16;
-        bv[j] = *reinterpret_cast<const half4*>(bias + (n < N ? n : N - 4));
+        if (n + 4 <= N) {
+          bv[j] = *reinterpret_cast<const half4*>(bias + n);
+        } else {
+          // bias holds exactly N entries
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            bv[j][e] = n + e < N ? __builtin_bit_cast(_Float16, bias[n + e]) : (_Float16)0;
+        }
       }
     }
 
@@ -485,8 +535,11 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
         const int64_t mc = m < M ? m : M - 1;
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
+          // a 4-column group that starts before N is read whole: rows are
+          // readable up to N rounded up to 8 (leading dimensions are
+          // multiples of 8)
           const int64_t n = nb + j * 16;
-          const int64_t nc = n < N ? n : N - 4;
+          const int64_t nc = n < N ? n : 0;
           if constexpr (EPI == 2) {
             in[ii][j][0] = *reinterpret_cast<const half4*>(X1 + mc * ldx1 + nc);
             in[ii][j][1] = *reinterpret_cast<const half4*>(X1 + mc * ldx1 + P + nc);
@@ -536,8 +589,19 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
         for (int j = 0; j < TN; ++j) {
           const int64_t n = nb + j * 16;
           if (m < M && n < N) {
-            *reinterpret_cast<half4*>(C + m * ldc + n) = out[ii][j][0];
-            if constexpr (EPI == 2) *reinterpret_cast<half4*>(C + m * ldc + P + n) = out[ii][j][1];
+            if (EPI == 2 || n + 4 <= N) {
+              *reinterpret_cast<half4*>(C + m * ldc + n) = out[ii][j][0];
+              if constexpr (EPI == 2)
+                *reinterpret_cast<half4*>(C + m * ldc + P + n) = out[ii][j][1];
+            } else {
+              // the last 1-3 columns of a ragged N (plain epilogue only),
+              // taken from the packed bits (the element-indexed form of
+              // these stores compiled to stores of element 0 only)
+              const uint64_t bits = __builtin_bit_cast(uint64_t, out[ii][j][0]);
+              C[m * ldc + n] = (lt_half)bits;
+              if (n + 1 < N) C[m * ldc + n + 1] = (lt_half)(bits >> 16);
+              if (n + 2 < N) C[m * ldc + n + 2] = (lt_half)(bits >> 32);
+            }
           }
         }
       }
@@ -552,11 +616,12 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   }
 }
 
-template <int BM, int BN, int WGM, int WGN, int BK, int NS, bool TA, bool TB, int EPI>
+template <int BM, int BN, int WGM, int WGN, int BK, int NS, bool TA, bool TB, int EPI,
+          bool RK = false>
 hipError_t launch(const GemmArgs& g, hipStream_t s, int splits = 1) {
   const int tiles_m = (int)((g.M + BM - 1) / BM);
   const int tiles_n = EPI == 1 ? (int)((g.F + BN / 2 - 1) / (BN / 2)) : (int)((g.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_f16_kernel<BM, BN, WGM, WGN, BK, NS, TA, TB, EPI>),
+  hipLaunchKernelGGL((gemm_f16_kernel<BM, BN, WGM, WGN, BK, NS, TA, TB, EPI, RK>),
                      dim3(tiles_m * tiles_n, splits), dim3(WGM * WGN * kWave), 0, s, g.M, g.N, g.K, g.alpha,
                      g.A, g.lda, g.B, g.ldb, g.beta, g.R, g.ldr, g.C, g.ldc, tiles_m, tiles_n, 8,
                      g.X1, g.ldx1, g.F, g.pair_off > 0 ? g.pair_off : g.F, g.bias);
@@ -654,6 +719,12 @@ hipError_t dispatch_tile(const GemmArgs& g, hipStream_t s) {
   const int64_t waves = big_tiles / kCUs, rem = big_tiles % kCUs;
   SplitTail st;
   if constexpr (EPI == 0) {
+    // K not a multiple of 8 (no layer shape): one launch of the tiles with
+    // the last slice's fix-up (256x256 from about one wave of them)
+    if (g.K & 7) {
+      if (big_tiles >= 192) return launch<256, 256, 2, 4, 64, 2, TA, TB, 0, true>(g, s);
+      return launch<128, 128, 2, 2, 64, 2, TA, TB, 0, true>(g, s);
+    }
     if (g.ws != nullptr && gemm_splitk_tail(g.M, g.N, g.K, &st) &&
         gemm_splitk_ws_bytes(g.M, g.N, g.K) <= g.ws_bytes) {
       // The last wave (or a launch of less than one wave) as split-K 256x256

@@ -114,7 +114,6 @@ static lt_status gemm_common(int transA, int transB, int64_t M, int64_t N, int64
     return fail(LT_ERR_INVALID_ARG, "lda/ldb smaller than the stored row length");
   if (ldc < N) return fail(LT_ERR_INVALID_ARG, "ldc %lld < N %lld", (long long)ldc, (long long)N);
   if (beta != 0.f && ldr < N) return fail(LT_ERR_INVALID_ARG, "ldr %lld < N %lld", (long long)ldr, (long long)N);
-  if ((M | N | K) & 7) return fail(LT_ERR_UNSUPPORTED, "M, N, K must be multiples of 8");
   if (((K > 0 ? (lda | ldb) : 0) | ldc | (beta != 0.f ? ldr : 0)) & 7)
     return fail(LT_ERR_UNSUPPORTED, "leading dimensions must be multiples of 8");
   if ((K > 0 && (!aligned16(A) || !aligned16(B))) || !aligned16(C) ||

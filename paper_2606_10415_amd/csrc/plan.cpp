@@ -16,6 +16,9 @@ bool gemm_splitk_tail(int64_t M, int64_t N, int64_t K, SplitTail* p) {
   // costs more than the larger tile saves
   constexpr int64_t kCUs = 256, kMinSlices = 8, kMaxSplits = 8, kLongK = 2048;
   if (M <= 0 || N <= 0 || K <= 0) return false;
+  // the partial tiles and their sum move 8 columns at a time, and a ragged K
+  // takes its own launch: both need multiples of 8
+  if ((N & 7) || (K & 7)) return false;
   // beyond the sizes the GEMM entry points accept: no plan (and no overflow)
   if (M > ((int64_t)1 << 30) || N > ((int64_t)1 << 30) || K > ((int64_t)1 << 30)) return false;
   const int64_t tm = (M + 255) / 256, tn = (N + 255) / 256, tiles = tm * tn;

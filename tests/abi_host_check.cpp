@@ -147,8 +147,20 @@ static void documented_cases() {
          LT_ERR_INVALID_ARG, "gemm A NULL");
   expect(lt_gemm_f16(0, 1, 64, 64, 64, 1.f, H, 32, H, 64, 0.f, H, 64, nullptr),
          LT_ERR_INVALID_ARG, "gemm lda");
-  expect(lt_gemm_f16(0, 1, 60, 64, 64, 1.f, H, 64, H, 64, 0.f, H, 64, nullptr),
-         LT_ERR_UNSUPPORTED, "gemm M % 8");
+  expect(lt_gemm_f16(0, 1, 64, 64, 64, 1.f, H, 64, H, 64, 0.f, H, 68, nullptr),
+         LT_ERR_UNSUPPORTED, "gemm ldc % 8");
+  expect(lt_gemm_f16(0, 1, ((int64_t)1 << 30) + 8, 64, 64, 1.f, H, 64, H, 64, 0.f, H, 64, nullptr),
+         LT_ERR_UNSUPPORTED, "gemm M > 2^30");
+  {
+    const int before = g_launches;
+    expect(lt_gemm_f16(1, 0, 61, 45, 13, 1.f, H, 64, H, 48, 0.f, H, 48, nullptr), LT_ERR_HIP,
+           "gemm ragged M, N, K reaches the launcher");
+    CHECK(g_launches == before + 1, "ragged gemm launcher not reached");
+    CHECK(lt_gemm_f16_workspace_size(0, 1, 4096, 22016 - 2048 + 4, 4096) == 0,
+          "no split-K workspace for N % 8 != 0");
+    CHECK(lt_gemm_f16_workspace_size(0, 1, 4096, 22016 - 2048, 4092) == 0,
+          "no split-K workspace for K % 8 != 0");
+  }
   expect(lt_gemm_f16(0, 1, 64, 64, 64, 1.f, off(H, 2), 64, H, 64, 0.f, H, 64, nullptr),
          LT_ERR_UNSUPPORTED, "gemm misaligned A");
   expect(lt_gemm_f16(0, 1, 64, 64, 64, 1.f, H, 1 << 22, H, 64, 0.f, H, 64, nullptr),

@@ -53,8 +53,8 @@ def _gemm(**kw):
     (dict(C=None), lt.LT_ERR_INVALID_ARG),
     (dict(lda=32), lt.LT_ERR_INVALID_ARG),
     (dict(ldc=8), lt.LT_ERR_INVALID_ARG),
-    (dict(M=60), lt.LT_ERR_UNSUPPORTED),
-    (dict(K=20, lda=20, ldb=20), lt.LT_ERR_UNSUPPORTED),
+    (dict(ldc=68), lt.LT_ERR_UNSUPPORTED),
+    (dict(M=(1 << 30) + 8), lt.LT_ERR_UNSUPPORTED),
     (dict(lda=68), lt.LT_ERR_UNSUPPORTED),
     (dict(A=FAKE + 2), lt.LT_ERR_UNSUPPORTED),
 ])
@@ -310,7 +310,7 @@ def test_gemm_bias_rejects_on_host():
         FAKE, 64, None)
     assert g(bias=None) == lt.LT_ERR_INVALID_ARG
     assert g(bias=FAKE + 2) == lt.LT_ERR_UNSUPPORTED
-    assert g(M=60) == lt.LT_ERR_UNSUPPORTED
+    assert g(M=(1 << 30) + 8) == lt.LT_ERR_UNSUPPORTED    # beyond the tile grid
     assert g(M=0, bias=None) == lt.LT_OK          # empty: no-op
 
 

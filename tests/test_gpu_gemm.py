@@ -81,6 +81,45 @@ def test_gemm_residual_operand_bitwise(env, transA, transB):
     assert np.array_equal(got.view(np.uint16), ref.view(np.uint16))
 
 
+def _padded(x, trans, fill):
+    """x stored (transposed if trans) with its leading dimension rounded up to
+    a multiple of 8; the padding holds `fill`."""
+    st = _stored(x, trans)
+    ld = -(-st.shape[1] // 8) * 8
+    out = np.full((st.shape[0], ld), fill, np.float16)
+    out[:, :st.shape[1]] = st
+    return out
+
+
+@pytest.mark.parametrize("transA,transB", LAYOUTS)
+@pytest.mark.parametrize("M,N,K", [(1, 1, 1), (61, 45, 13), (130, 44, 70), (257, 263, 77),
+                                   # 256x256 tiles with the ragged-K fix-up in the slice loop
+                                   (3000, 4100, 515)])
+def test_gemm_ragged_sizes_bitwise(env, transA, transB, M, N, K):
+    """M, N, K not multiples of 8, leading dimensions padded to 8: the padding
+    of A, B and R holds NaN (it must never reach a stored result), the padding
+    of C a sentinel (it must not be written)."""
+    torch, lt = env
+    print(f"gemm ragged trans=({transA},{transB}) M={M} N={N} K={K}", flush=True)
+    a = uniform_int_f16(21, (M, K), -2, 2)
+    b = uniform_int_f16(22, (K, N), -2, 2)
+    r = uniform_int_f16(23, (M, N), -8, 8)
+    bias = uniform_int_f16(24, (N,), -4, 4)
+    A = torch.from_numpy(_padded(a, transA, np.nan)).cuda()
+    B = torch.from_numpy(_padded(b, transB, np.nan)).cuda()
+    R = torch.from_numpy(_padded(r, 0, np.nan)).cuda()
+    sentinel = np.float16(12345.0)
+    C = torch.from_numpy(_padded(np.full((M, N), np.nan, np.float16), 0, sentinel)).cuda()
+    Bias = torch.from_numpy(bias).cuda()
+    lt.lt_gemm_f16_bias(transA, transB, M, N, K, 3.0, A, A.shape[1], B, B.shape[1], -2.0, R,
+                        R.shape[1], Bias, C, C.shape[1])
+    torch.cuda.synchronize()
+    got = C.cpu().numpy()
+    ref = (oracle.gemm(0, 0, 3.0, a, b, -2.0, r) + bias.astype(np.float64)).astype(np.float16)
+    assert np.array_equal(got[:, :N].view(np.uint16), ref.view(np.uint16))
+    assert (got[:, N:] == sentinel).all()
+
+
 def test_gemm_beta_zero_ignores_nan_and_k_zero(env):
     torch, lt = env
     a = normal_f16(7, (64, 32))
