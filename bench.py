@@ -45,11 +45,12 @@ GEMM_TRAFFIC = {
     "workload": "llama2-7b",
     "layer": "paper",
     "fuse_swiglu": True,
-    "sources_sha256": "c4d454f978e0802ef87dd5dcb1d6886726658401e62d0402a4a84ec4f793d469",
-    "fetch_bytes_per_launch": 664103038,
-    "write_bytes_per_launch": 99974501,
+    "sources_sha256": "980fbbb9e74475907d8dd9f0ef2443a73e59870bfbf7691b3ea679014a45e9bf",
+    "fetch_bytes_per_launch": 664182705,
+    "write_bytes_per_launch": 100067587,
 }
-GEMM_SOURCES = ("paper_2606_10415_amd/csrc/gemm_f16.hip", "paper_2606_10415_amd/csrc/common.hpp")
+GEMM_SOURCES = ("paper_2606_10415_amd/csrc/gemm_f16.hip", "paper_2606_10415_amd/csrc/common.hpp",
+                "paper_2606_10415_amd/csrc/plan.cpp")
 
 
 def gemm_sources_sha256():
@@ -153,7 +154,9 @@ def sweep():
 
     * attention forward / backward at the sequence lengths of the paper's
       attention-BP comparison (LLaMA-2-7B heads at S = 1024, 2048, 4096;
-      Qwen2.5-32B heads at S = 2048), B = 1, causal;
+      Qwen2.5-32B heads at S = 2048), B = 1, causal: the default pair
+      (lt_attn_fwd, then lt_attn_bwd recomputing P) beside the saved-P pair
+      of Algorithm 1 (lt_attn_fwd_p stores P, lt_attn_bwd_p reads it);
     * the paper's representative GEMM shapes (Sec. 6.6, Table "Representative
       FP16 GEMM backend profile", sequence length 2048): M = 2048 tokens,
       K x N = 4096x4096, 4096x11008, 11008x4096, 6656x6656, 8192x8192, as the
@@ -210,11 +213,26 @@ def sweep():
         fwd()
         pairs = S * (S + 1) // 2 * Hq * B
         tf, tb = timed(fwd), timed(bwd)
+        # saved P (its own workspace; P is 2 bytes per kept (query, key) pair)
+        pbytes = lt.lt_attn_p_size(B, S, Hq, 1)
+        P = torch.empty(pbytes, dtype=torch.uint8, device="cuda")
+        wpb = lt.lt_attn_bwd_p_workspace_size(B, S, Hq, Hkv, D)
+        wsp = torch.empty(wpb, dtype=torch.uint8, device="cuda")
+        fwdp = lambda: lt.lt_attn_fwd_p(q, k, v, W, W, O, Hq * D, LSE, P, pbytes, B, S, Hq, Hkv, D,
+                                        sc, 1)
+        bwdp = lambda: lt.lt_attn_bwd_p(q, k, v, W, W, O, dO, Hq * D, LSE, P, pbytes, dq, dk, dv,
+                                        W, W, wsp, wpb, B, S, Hq, Hkv, D, sc, 1)
+        fwdp()
+        tfp, tbp = timed(fwdp), timed(bwdp)
         emit({"sweep": "attention", "workload": name, "B": B, "S": S, "Hq": Hq, "Hkv": Hkv, "D": D,
               "fwd_ms": round(tf, 4), "fwd_tflops": round(4 * D * pairs / tf / 1e9, 1),
               "bwd_ms": round(tb, 4), "bwd_tflops": round(8 * D * pairs / tb / 1e9, 1),
-              "bwd_frac_peak": round(8 * D * pairs / tb / 1e9 / PEAK_FP16_TFLOPS, 4)})
-        del QKV, dO, O, dQKV, ws
+              "bwd_frac_peak": round(8 * D * pairs / tb / 1e9 / PEAK_FP16_TFLOPS, 4),
+              "saved_p": {"fwd_p_ms": round(tfp, 4), "bwd_p_ms": round(tbp, 4),
+                          "p_mib": round(pbytes / 2**20, 1),
+                          "fwd_bwd_ms": round(tfp + tbp, 4),
+                          "recompute_fwd_bwd_ms": round(tf + tb, 4)}})
+        del QKV, dO, O, dQKV, ws, P, wsp
 
     M = 2048
     for K, N in [(4096, 4096), (4096, 11008), (11008, 4096), (6656, 6656), (8192, 8192)]:
