@@ -52,6 +52,24 @@
 namespace lt {
 namespace {
 
+// Direct load of 16 bytes per lane into LDS, as lds_dma16_opaque, for data
+// read once (non-temporal: the line is not kept in the caches for reuse, so
+// it does not evict the operands that are).
+__device__ __forceinline__ void lds_dma16_stream(const void* base, uint32_t nrec, void* lds,
+                                                 uint32_t voff) {
+  const uint64_t b = (uint64_t)base;
+  u32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((uint32_t)b);
+  r[1] = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32) & 0xffffu);
+  r[2] = __builtin_amdgcn_readfirstlane(nrec);
+  r[3] = 0x00020000u;
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen nt lds"
+               :
+               : "s"(m0v), "v"(voff), "s"(r)
+               : "memory");
+}
+
 constexpr int NWA = 8;         // dK/dV: waves per workgroup
 constexpr int BKV = NWA * 32;  // dK/dV: keys per workgroup (32 per wave)
 constexpr int BQA = 64;        // dK/dV: queries per block (two 32-query halves)
@@ -499,8 +517,11 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
                                    : (int64_t)qg * ((S + 31) >> 5) + kgi;
         char* dst = reinterpret_cast<char*>(ds_out) +
                     (((int64_t)b * Hq + h) * nblk + blk) * kDsBlockBytes + lane * 32;
-        st16(dst, as_u32x4(pds[0]));
-        st16(dst + 16, as_u32x4(pds[1]));
+        // written once, read once by the dQ pass: non-temporal, so that the
+        // 2 KiB blocks (0.5 GB per call at S = 4096) do not evict the Q / dO
+        // blocks and K / V tiles the key tiles share through L2
+        __builtin_nontemporal_store(as_u32x4(pds[0]), reinterpret_cast<u32x4*>(dst));
+        __builtin_nontemporal_store(as_u32x4(pds[1]), reinterpret_cast<u32x4*>(dst + 16));
       }
       __builtin_amdgcn_s_setprio(1);
 #pragma unroll
@@ -693,8 +714,8 @@ attn_bwd_dq_kernel(const lt_half* __restrict__ K, int64_t kv_stride, const lt_ha
       const int kg = 2 * ks + c;
       const char* src = dsq + (int64_t)(kg < kg_end ? kg : 0) * kDsBlockBytes;
       const uint32_t nrec = kg < kg_end ? kDsBlockBytes : 0u;
-      lds_dma16_opaque(src, nrec, mine + c * kDsBlockBytes, (uint32_t)(lane * 16));
-      lds_dma16_opaque(src, nrec, mine + c * kDsBlockBytes + 1024, (uint32_t)(1024 + lane * 16));
+      lds_dma16_stream(src, nrec, mine + c * kDsBlockBytes, (uint32_t)(lane * 16));
+      lds_dma16_stream(src, nrec, mine + c * kDsBlockBytes + 1024, (uint32_t)(1024 + lane * 16));
     }
   };
 
