@@ -111,10 +111,10 @@ attn_save_p_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lrow = lane & 31;
   const int g = lane >> 5;
-  const int bh = blockIdx.x % (B * Hq);
   const int jt = blockIdx.x / (B * Hq);            // ascending key tile = descending work
-  const int b = bh / Hq;
-  const int h = bh % Hq;
+  int b, h;
+  query_head(blockIdx.x % (B * Hq), B, Hq, Hkv, b, h);
+  const int bh = b * Hq + h;
   const int kvh = h / (Hq / Hkv);
   const int kbase = jt * BKV;
   const int kw0 = kbase + wave * 32;
@@ -680,10 +680,10 @@ attn_bwd_dq_kernel(const lt_half* __restrict__ K, int64_t kv_stride, const lt_ha
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int n32 = (S + 31) / 32;
   const int n_qt = (S + BQQ - 1) / BQQ;
-  const int bh = blockIdx.x % (B * Hq);
   const int qt = causal ? n_qt - 1 - (int)(blockIdx.x / (B * Hq)) : (int)(blockIdx.x / (B * Hq));
-  const int b = bh / Hq;
-  const int h = bh % Hq;
+  int b, h;
+  query_head(blockIdx.x % (B * Hq), B, Hq, Hkv, b, h);
+  const int bh = b * Hq + h;
   const int kvh = h / (Hq / Hkv);
   const int qg = qt * NWQ + wave;                  // this wave's 32-query group
   // key groups this wave takes: 0 .. kg_end - 1 (those the mask keeps)
@@ -811,10 +811,9 @@ attn_bwd_dq_recompute_kernel(const lt_half* __restrict__ Q, const lt_half* __res
   const int kpart = wave / NQG;                    // which of the QSPLIT key-block shares
 
   const int n_qt = (S + BQ - 1) / BQ;
-  const int bh = blockIdx.x % (B * Hq);
   const int qt = causal ? n_qt - 1 - (int)(blockIdx.x / (B * Hq)) : (int)(blockIdx.x / (B * Hq));
-  const int b = bh / Hq;
-  const int h = bh % Hq;
+  int b, h;
+  query_head(blockIdx.x % (B * Hq), B, Hq, Hkv, b, h);
   const int kvh = h / (Hq / Hkv);
   const int q0 = qt * BQ;
   const int qw0 = q0 + qg * 32;

@@ -83,10 +83,9 @@ attn_fwd_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
   const int kpart = wave / NQG;                    // which block of each slice (QSPLIT = 2)
 
   const int n_qt = (S + BQW - 1) / BQW;
-  const int bh = blockIdx.x % (B * Hq);
   const int qt = causal ? n_qt - 1 - (int)(blockIdx.x / (B * Hq)) : (int)(blockIdx.x / (B * Hq));
-  const int b = bh / Hq;
-  const int h = bh % Hq;
+  int b, h;
+  query_head(blockIdx.x % (B * Hq), B, Hq, Hkv, b, h);
   const int kvh = h / (Hq / Hkv);
   const int q0 = qt * BQW;
   const int qw0 = q0 + qg * 32;

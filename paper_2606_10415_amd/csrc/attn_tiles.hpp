@@ -62,4 +62,22 @@ struct RowTile {
   }
 };
 
+// (b, h) of a query-head workgroup from bh = blockIdx.x % (B * Hq).  The
+// hardware deals consecutive workgroups to the 8 XCDs in turn, so bh's
+// residue mod 8 picks the XCD (B * Hq is then a multiple of 8).  With
+// grouped queries and B * Hkv a multiple of 8, the Hq / Hkv query heads of
+// one kv head get bh values equal mod 8: they run on one XCD and read their
+// shared K / V tiles through one L2.  Otherwise heads follow bh in order.
+__device__ __forceinline__ void query_head(int bh, int B, int Hq, int Hkv, int& b, int& h) {
+  if (Hq != Hkv && (B * Hkv) % 8 == 0) {
+    const int bkv = bh % (B * Hkv);
+    const int j = bh / (B * Hkv);
+    b = bkv / Hkv;
+    h = (bkv % Hkv) * (Hq / Hkv) + j;
+  } else {
+    b = bh / Hq;
+    h = bh % Hq;
+  }
+}
+
 }  // namespace lt
