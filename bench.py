@@ -46,8 +46,8 @@ GEMM_TRAFFIC = {
     "layer": "paper",
     "fuse_swiglu": True,
     "sources_sha256": "980fbbb9e74475907d8dd9f0ef2443a73e59870bfbf7691b3ea679014a45e9bf",
-    "fetch_bytes_per_launch": 664182705,
-    "write_bytes_per_launch": 100067587,
+    "fetch_bytes_per_launch": 664285414,
+    "write_bytes_per_launch": 99802084,
 }
 GEMM_SOURCES = ("paper_2606_10415_amd/csrc/gemm_f16.hip", "paper_2606_10415_amd/csrc/common.hpp",
                 "paper_2606_10415_amd/csrc/plan.cpp")
