@@ -648,7 +648,10 @@ struct DqSmem {
 // 32 bytes per lane of the dK/dV pass, see attn_bwd_ds_blocks): lane L gets
 // stored query position L % 32 at keys kb + 8 (j / 4) + 4 (L / 32) + j % 4,
 // j = 0..7 (the key order of RowTile::tr_frag<true>).  Each 16-lane group
-// reads four consecutive 32-byte lanes: no bank conflicts.
+// reads four consecutive 32-byte lanes; the two groups of one 32-lane read
+// cycle are 1 KiB apart and share their banks (a two-way conflict).  The
+// pass is bound by the dS stream: a 128-byte gap between the block halves,
+// which removes the conflict, measured level.
 __device__ __forceinline__ half8 ds_tr_frag(const char* blk, int kb, int lane) {
   v4s part[2];
 #pragma unroll
