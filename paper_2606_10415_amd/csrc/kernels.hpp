@@ -167,7 +167,7 @@ inline size_t attn_bwd_part_bytes(int B, int S, int Hq, int Hkv, int D) {
 }
 
 // RMSNorm backward (norm_rope.hip).  dW partial sums: one FP32 row of H per
-// workgroup (8 waves), rmsnorm_bwd_blocks(T) workgroups.
+// workgroup (4 waves), rmsnorm_bwd_blocks(T) workgroups.
 struct RmsBwdArgs {
   const lt_half* dY;
   int64_t lddy;
@@ -184,9 +184,12 @@ struct RmsBwdArgs {
   int64_t T, H;
 };
 constexpr int kRmsBwdWaves = 4;
-inline int rmsnorm_bwd_blocks(int64_t T) {   // about one row per wave, at most 1024 workgroups
+// One row per wave up to 2048 rows, then at most 512 workgroups (two rows per
+// wave at T = 4096): a wave's second row loads while other waves store their
+// first, and the dW pass has half the partial rows of one row per wave.
+inline int rmsnorm_bwd_blocks(int64_t T) {
   const int64_t b = T / kRmsBwdWaves + (T % kRmsBwdWaves != 0);   // no overflow at any T
-  return (int)(b < 1024 ? (b < 1 ? 1 : b) : 1024);
+  return (int)(b < 512 ? (b < 1 ? 1 : b) : 512);
 }
 inline size_t rmsnorm_bwd_ws_bytes(int64_t T, int64_t H) {
   return align256((size_t)rmsnorm_bwd_blocks(T) * H * sizeof(float));

@@ -6,8 +6,9 @@
 //     l, l + 64, ... of the row (coalesced), the sum of squares is a wave
 //     shuffle reduction; writes y = w * x * r (one rounding) and r.
 //       r = (mean_j x_j^2 + eps)^(-1/2)
-//   * rmsnorm_bwd: the same row layout, 4 waves per workgroup, about one row
-//     per wave; per row
+//   * rmsnorm_bwd: the same row layout, 4 waves per workgroup, one row per
+//     wave for short inputs and a few for long ones (at most 512
+//     workgroups); per row
 //       dx = r * w * g - r^3 * x / H * sum_j g_j w_j x_j   (+ residual R)
 //     with g and x held in registers between the row dot product and dx
 //     (rows up to 6144 columns; wider rows are read twice, the second time

@@ -219,8 +219,8 @@ def test_rmsnorm_fwd_rejects_on_host(kw, status):
 def test_rmsnorm_empty_is_noop_and_workspace():
     assert _rms_fwd(T=0) == lt.LT_OK
     ws = lt.lt_rmsnorm_bwd_workspace_size(4096, 4096)
-    # min(ceil(T / 4), 1024) = 1024 workgroups x one FP32 row of H partial sums
-    assert ws == 1024 * 4096 * 4
+    # min(ceil(T / 4), 512) = 512 workgroups x one FP32 row of H partial sums
+    assert ws == 512 * 4096 * 4
     assert lt.lt_rmsnorm_bwd_workspace_size(77, 5120) == 20 * 5120 * 4     # ceil(77 / 4) rows
     assert lt.lt_rmsnorm_bwd_workspace_size(3, 8) % 256 == 0
     assert lt.lt_rmsnorm_bwd_workspace_size(0, 8) == 0

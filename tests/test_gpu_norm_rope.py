@@ -32,7 +32,7 @@ def env():
 
 @pytest.mark.parametrize("T,H,residual", [(77, 5120, True), (256, 256, False), (4096, 4096, True),
                                           (3, 8192, True), (1, 8, False),
-                                          # more rows than 4 x 1024: several rows per wave
+                                          # more rows than 4 x 512: several rows per wave
                                           (8200, 256, True), (4100, 5120, True)])
 def test_rmsnorm_parity(env, T, H, residual):
     print(f"rmsnorm T={T} H={H} residual={residual}", flush=True)
