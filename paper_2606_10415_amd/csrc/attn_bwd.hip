@@ -45,6 +45,8 @@
 // with the recomputed S); the dS round trip through HBM replaces both the
 // second S / dP recompute of a query-major dQ pass and dQ atomics.
 
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "attn_tiles.hpp"
@@ -201,14 +203,17 @@ template <int D>
 struct DkdvSmem {
   using RT = RowTile<D, NWA>;
   static constexpr int TQ = BQA * RT::ROWB;             // one Q or dO block
-  static constexpr int V_OFF = 0;                        // V tile [BKV][D]
-  static constexpr int Q_OFF = V_OFF + BKV * RT::ROWB;   // 2 buffers
+  // Q and dO buffers first: every fragment read of them is a per-lane
+  // register plus a constant below 64 KiB (the LDS instructions' offset field)
+  static constexpr int Q_OFF = 0;                        // 2 buffers
   static constexpr int DO_OFF = Q_OFF + 2 * TQ;          // 2 buffers
   // base-2 LSE and D rows: 2 buffers x {LSE2, D} x 256 B (one 4-byte direct
   // load of 64 lanes each)
   static_assert(BQA == 64, "one 4-byte direct load per row vector");
   static constexpr int ROW_OFF = DO_OFF + 2 * TQ;
-  static constexpr int BYTES = ROW_OFF + 4 * 256;
+  static constexpr int V_OFF = ROW_OFF + 4 * 256;        // V tile [BKV][D]
+  static_assert(DO_OFF + 2 * TQ <= 65536, "Q / dO offsets fit the offset field");
+  static constexpr int BYTES = V_OFF + BKV * RT::ROWB;
 };
 
 // KSPLIT = 1: 8 key groups of 32 (256 keys), every wave walks both 32-query
@@ -271,6 +276,13 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
   for (int kk = 0; kk < KK; ++kk)
     kf[kk] = mykey < S ? as_half8(ld16((SP ? Vp : Kp) + (int64_t)mykey * kv_stride + kk * 16 + g * 8))
                        : as_half8(u32x4{0, 0, 0, 0});
+
+  // lane part of the row-fragment address of step kk (rows rb + lane % 32,
+  // rb a multiple of 16, so the swizzle depends on the lane only)
+  uint32_t rlane[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) rlane[kk] = (uint32_t)RT::addr(lane & 31, kk * 2 + (lane >> 5));
+  const uint32_t vrow0 = __builtin_amdgcn_readfirstlane(SM::V_OFF + kg * 32 * RT::ROWB);
 
   f32x16 dkacc[DB], dvacc[DB];
 #pragma unroll
@@ -365,8 +377,9 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
     }
   }
 
-  for (int it = 0; it < n_iter; ++it) {
-    const int cur = it & 1;
+  // two block iterations per trip, so that the buffer index is a constant
+  auto iteration = [&](int it, auto CUR_) {
+    const int cur = CUR_;   // a constant in the unrolled main path
     int h, qbase;
     block_of(it, h, qbase);
     // that buffer was last read before the previous barrier
@@ -379,8 +392,7 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
     const float* lse_s = reinterpret_cast<const float*>(smem + SM::ROW_OFF + cur * 512);
     const float* del_s = reinterpret_cast<const float*>(smem + SM::ROW_OFF + cur * 512 + 256);
 
-#pragma nounroll
-    for (int ih = 0; ih < BQA / 32 / KSPLIT; ++ih) {
+    auto half = [&](int ih) {
     const int hq = KSPLIT > 1 ? kpart : ih;
     // 32-query half hq of the block; causal: all of this wave's keys after
     // all of its queries -> P = 0
@@ -448,18 +460,34 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
         sacc[r] = 0.f;
         pacc[r] = 0.f;
       }
-      // fragments of step kk+1 are read before the MFMAs of step kk
-      half8 fq = RT::row_frag(qs, hq * 32, 0, lane);
-      half8 fd = RT::row_frag(dos, hq * 32, 0, lane);
-      half8 fv = RT::row_frag(smem + SM::V_OFF, kg * 32, 0, lane);
+      // fragments of step kk+1 are read before the MFMAs of step kk; the Q
+      // and dO reads are a lane register plus a constant, the V read's address
+      // is added right before it (kept there: holding eight V addresses
+      // through the loop does not fit the register budget)
+      auto rdq = [&](int kk) {
+        return as_half8(*reinterpret_cast<const u32x4*>(smem + SM::Q_OFF + cur * SM::TQ +
+                                                        hq * 32 * RT::ROWB + rlane[kk]));
+      };
+      auto rdo = [&](int kk) {
+        return as_half8(*reinterpret_cast<const u32x4*>(smem + SM::DO_OFF + cur * SM::TQ +
+                                                        hq * 32 * RT::ROWB + rlane[kk]));
+      };
+      auto rdv = [&](int kk) {
+        uint32_t a;
+        asm volatile("v_add_u32 %0, %1, %2" : "=v"(a) : "v"(rlane[kk]), "s"(vrow0));
+        return as_half8(*reinterpret_cast<const u32x4*>(smem + a));
+      };
+      half8 fq = rdq(0);
+      half8 fd = rdo(0);
+      half8 fv = rdv(0);
       __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
         half8 nq = fq, nd = fd, nv = fv;
         if (kk + 1 < KK) {
-          nq = RT::row_frag(qs, hq * 32, kk + 1, lane);
-          nd = RT::row_frag(dos, hq * 32, kk + 1, lane);
-          nv = RT::row_frag(smem + SM::V_OFF, kg * 32, kk + 1, lane);
+          nq = rdq(kk + 1);
+          nd = rdo(kk + 1);
+          nv = rdv(kk + 1);
         }
         sacc = mfma32(fq, kf[kk], sacc);
         pacc = mfma32(fd, fv, pacc);
@@ -535,6 +563,13 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
         }
       __builtin_amdgcn_s_setprio(0);
     }
+    };
+    if constexpr (KSPLIT == 1 && !SP) {
+#pragma unroll
+      for (int ih = 0; ih < BQA / 32; ++ih) half(ih);
+    } else {
+#pragma nounroll
+      for (int ih = 0; ih < BQA / 32 / KSPLIT; ++ih) half(ih);
     }
 
     // next block resident for every wave; nobody reads this buffer any more
@@ -547,6 +582,14 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
         pcur[ih][1] = pnxt[ih][1];
       }
     }
+  };
+  if constexpr (KSPLIT == 1) {
+    for (int it = 0; it < n_iter; it += 2) {
+      iteration(it, std::integral_constant<int, 0>{});
+      if (it + 1 < n_iter) iteration(it + 1, std::integral_constant<int, 1>{});
+    }
+  } else {
+    for (int it = 0; it < n_iter; ++it) iteration(it, it & 1);
   }
 
   if constexpr (KSPLIT > 1) {
