@@ -28,6 +28,8 @@
 //     probabilities then stay below 256, well inside FP16, and most slices
 //     skip the rescale entirely.
 
+#include <type_traits>
+
 #include "common.hpp"
 #include "kernels.hpp"
 #include "attn_tiles.hpp"
@@ -106,6 +108,12 @@ attn_fwd_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
       qf[kk] = myq < S ? as_half8(ld16(qp + kk * 16)) : as_half8(u32x4{0, 0, 0, 0});
   }
 
+  // lane part of the K row-fragment address of step kk (rows rb + lane % 32,
+  // rb a multiple of 16, so the swizzle depends on the lane only)
+  uint32_t rlane[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) rlane[kk] = (uint32_t)RT::addr(lane & 31, kk * 2 + (lane >> 5));
+
   f32x16 oacc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db)
@@ -136,10 +144,13 @@ attn_fwd_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
   // workgroups of a CU then alternate between loading and computing); with
   // grouped queries, whose K/V slices hit L2 more often, it is 2-3.5% slower.
 
-  for (int kt = 0; kt < n_kv; ++kt) {
-    const char* st = smem + (kt & 1) * SM::STAGE;
+  // two slices per trip, so that the stage index is a constant and every LDS
+  // fragment address is a per-lane register plus the instruction's offset
+  auto slice = [&](int kt, auto CUR_) {
+    constexpr int cur = decltype(CUR_)::value;
+    const char* st = smem + cur * SM::STAGE;
     // that stage was last read before the previous barrier
-    if (kt + 1 < n_kv) stage_load(kt + 1, (kt + 1) & 1);
+    if (kt + 1 < n_kv) stage_load(kt + 1, cur ^ 1);
 
     const int key0 = kt * BKV;
     // QSPLIT = 2: this wave's block, skipped when wholly above its queries
@@ -155,23 +166,34 @@ attn_fwd_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
 #pragma unroll
         for (int r = 0; r < 16; ++r) sacc[kb][r] = 0.f;
       // K fragments of step kk+1 are read before the MFMAs of step kk
-      half8 kfr[KBW];
+      // (QSPLIT = 1: a per-lane register plus a constant; QSPLIT = 2 adds the
+      // wave's block offset)
+      auto rdk = [&](int kb, int kk) {
+        return as_half8(*reinterpret_cast<const u32x4*>(
+            st + (kb0 + kb * 32) * RT::ROWB + rlane[kk]));
+      };
+      // two register sets by step parity, so that step kk+1's reads do not
+      // wait for step kk's MFMAs to release their registers
+      half8 kfr[2][KBW];
 #pragma unroll
-      for (int kb = 0; kb < KBW; ++kb) kfr[kb] = RT::row_frag(st, kb0 + kb * 32, 0, lane);
+      for (int kb = 0; kb < KBW; ++kb) kfr[0][kb] = rdk(kb, 0);
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
-        half8 nxt[KBW];
-#pragma unroll
-        for (int kb = 0; kb < KBW; ++kb)
-          nxt[kb] = kk + 1 < KK ? RT::row_frag(st, kb0 + kb * 32, kk + 1, lane) : kfr[kb];
-#pragma unroll
-        for (int kb = 0; kb < KBW; ++kb) sacc[kb] = mfma32(kfr[kb], qf[kk], sacc[kb]);
         if (kk + 1 < KK) {
-          __builtin_amdgcn_sched_group_barrier(0x100, KBW, 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, KBW, 0);
+#pragma unroll
+          for (int kb = 0; kb < KBW; ++kb) kfr[(kk + 1) & 1][kb] = rdk(kb, kk + 1);
         }
 #pragma unroll
-        for (int kb = 0; kb < KBW; ++kb) kfr[kb] = nxt[kb];
+        for (int kb = 0; kb < KBW; ++kb) sacc[kb] = mfma32(kfr[kk & 1][kb], qf[kk], sacc[kb]);
+        // the scheduling groups count from the top of the block: the first
+        // read group holds step 0's reads and step 1's
+        if (kk + 1 < KK) {
+          if (kk == 0)
+            __builtin_amdgcn_sched_group_barrier(0x100, 2 * KBW, 0);
+          else
+            __builtin_amdgcn_sched_group_barrier(0x100, KBW, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, KBW, 0);
+        }
       }
 
       // ---- mask (key > query, or key past S), row max ----
@@ -238,6 +260,10 @@ attn_fwd_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ K,
     // next slice resident for every wave; nobody reads this stage any more
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+  };
+  for (int kt = 0; kt < n_kv; kt += 2) {
+    slice(kt, std::integral_constant<int, 0>{});
+    if (kt + 1 < n_kv) slice(kt + 1, std::integral_constant<int, 1>{});
   }
 
   if constexpr (QSPLIT > 1) {
