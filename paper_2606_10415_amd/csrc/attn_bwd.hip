@@ -552,15 +552,32 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
         __builtin_nontemporal_store(as_u32x4(pds[1]), reinterpret_cast<u32x4*>(dst + 16));
       }
       __builtin_amdgcn_s_setprio(1);
+      // steps (kc, db): the transposed dO and Q fragments of step s + 1 are
+      // read before step s's two MFMAs, into the other of two register sets
+      constexpr int NST = 2 * DB;
+      half8 tdo[2], tq[2];
+      auto rd_tr = [&](int st_, half8& a, half8& b) {
+        const int kc = st_ / DB, db = st_ % DB;
+        a = RT::template tr_frag<true>(dos, hq * 32 + kc * 16, db * 32, lane);
+        b = RT::template tr_frag<true>(qs, hq * 32 + kc * 16, db * 32, lane);
+      };
+      rd_tr(0, tdo[0], tq[0]);
 #pragma unroll
-      for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          dvacc[db] = mfma32(RT::template tr_frag<true>(dos, hq * 32 + kc * 16, db * 32, lane),
-                             pp[kc], dvacc[db]);
-          dkacc[db] = mfma32(RT::template tr_frag<true>(qs, hq * 32 + kc * 16, db * 32, lane),
-                             pds[kc], dkacc[db]);
+      for (int st_ = 0; st_ < NST; ++st_) {
+        const int kc = st_ / DB, db = st_ % DB;
+        if (st_ + 1 < NST) rd_tr(st_ + 1, tdo[(st_ + 1) & 1], tq[(st_ + 1) & 1]);
+        dvacc[db] = mfma32(tdo[st_ & 1], pp[kc], dvacc[db]);
+        dkacc[db] = mfma32(tq[st_ & 1], pds[kc], dkacc[db]);
+        // the groups count from the top of the block: the first read group
+        // holds steps 0 and 1 (two transposed reads per fragment)
+        if (st_ + 1 < NST) {
+          if (st_ == 0)
+            __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+          else
+            __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
         }
+      }
       __builtin_amdgcn_s_setprio(0);
     }
     };
