@@ -393,193 +393,193 @@ attn_bwd_dkdv_kernel(const lt_half* __restrict__ Q, const lt_half* __restrict__ 
     const float* del_s = reinterpret_cast<const float*>(smem + SM::ROW_OFF + cur * 512 + 256);
 
     auto half = [&](int ih) {
-    const int hq = KSPLIT > 1 ? kpart : ih;
-    // 32-query half hq of the block; causal: all of this wave's keys after
-    // all of its queries -> P = 0
-    const int qh = qbase + hq * 32;
-    const bool active = (!causal || kw0 <= qh + 31) && kw0 < S;
-    if (SP && active) {
-      //   dP = dO V^T   (lane owns key `mykey`, 16 query rows; V fragments in registers)
-      //   dS = P (dP - D) with the saved P,  dV^T += dO^T P,  dK^T += Q^T dS
-      f32x16 pacc;
+      const int hq = KSPLIT > 1 ? kpart : ih;
+      // 32-query half hq of the block; causal: all of this wave's keys after
+      // all of its queries -> P = 0
+      const int qh = qbase + hq * 32;
+      const bool active = (!causal || kw0 <= qh + 31) && kw0 < S;
+      if (SP && active) {
+        //   dP = dO V^T   (lane owns key `mykey`, 16 query rows; V fragments in registers)
+        //   dS = P (dP - D) with the saved P,  dV^T += dO^T P,  dK^T += Q^T dS
+        f32x16 pacc;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) pacc[r] = 0.f;
-      half8 fd = RT::row_frag(dos, hq * 32, 0, lane);
-      __builtin_amdgcn_s_setprio(1);
+        for (int r = 0; r < 16; ++r) pacc[r] = 0.f;
+        half8 fd = RT::row_frag(dos, hq * 32, 0, lane);
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        half8 nd = fd;
-        if (kk + 1 < KK) nd = RT::row_frag(dos, hq * 32, kk + 1, lane);
-        pacc = mfma32(fd, kf[kk], pacc);
-        fd = nd;
+        for (int kk = 0; kk < KK; ++kk) {
+          half8 nd = fd;
+          if (kk + 1 < KK) nd = RT::row_frag(dos, hq * 32, kk + 1, lane);
+          pacc = mfma32(fd, kf[kk], pacc);
+          fd = nd;
+        }
+        __builtin_amdgcn_s_setprio(0);
+        const half8* pp = pcur[0];   // this half's P (the halves are shifted down below)
+        float ds[16];
+#pragma unroll
+        for (int rq = 0; rq < 4; ++rq) {
+          const float4 d4 = *reinterpret_cast<const float4*>(del_s + hq * 32 + 8 * rq + 4 * g);
+          const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int r = 4 * rq + e;
+            ds[r] = (float)pp[r >> 3][r & 7] * (pacc[r] - dv[e]);
+          }
+        }
+        half8 pds[2];
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc)
+          pds[kc] = pack8(ds[8 * kc], ds[8 * kc + 1], ds[8 * kc + 2], ds[8 * kc + 3],
+                          ds[8 * kc + 4], ds[8 * kc + 5], ds[8 * kc + 6], ds[8 * kc + 7]);
+        __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            dvacc[db] = mfma32(RT::template tr_frag<true>(dos, hq * 32 + kc * 16, db * 32, lane),
+                               pp[kc], dvacc[db]);
+            dkacc[db] = mfma32(RT::template tr_frag<true>(qs, hq * 32 + kc * 16, db * 32, lane),
+                               pds[kc], dkacc[db]);
+          }
+        __builtin_amdgcn_s_setprio(0);
       }
-      __builtin_amdgcn_s_setprio(0);
-      const half8* pp = pcur[0];   // this half's P (the halves are shifted down below)
-      float ds[16];
+      if constexpr (SP && NH > 1) {   // next half's P into pcur[0] (constant register indices)
 #pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        const float4 d4 = *reinterpret_cast<const float4*>(del_s + hq * 32 + 8 * rq + 4 * g);
-        const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = 4 * rq + e;
-          ds[r] = (float)pp[r >> 3][r & 7] * (pacc[r] - dv[e]);
+        for (int j = 0; j + 1 < NH; ++j) {
+          pcur[j][0] = pcur[j + 1][0];
+          pcur[j][1] = pcur[j + 1][1];
         }
       }
-      half8 pds[2];
-#pragma unroll
-      for (int kc = 0; kc < 2; ++kc)
-        pds[kc] = pack8(ds[8 * kc], ds[8 * kc + 1], ds[8 * kc + 2], ds[8 * kc + 3],
-                        ds[8 * kc + 4], ds[8 * kc + 5], ds[8 * kc + 6], ds[8 * kc + 7]);
-      __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-      for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          dvacc[db] = mfma32(RT::template tr_frag<true>(dos, hq * 32 + kc * 16, db * 32, lane),
-                             pp[kc], dvacc[db]);
-          dkacc[db] = mfma32(RT::template tr_frag<true>(qs, hq * 32 + kc * 16, db * 32, lane),
-                             pds[kc], dkacc[db]);
-        }
-      __builtin_amdgcn_s_setprio(0);
-    }
-    if constexpr (SP && NH > 1) {   // next half's P into pcur[0] (constant register indices)
-#pragma unroll
-      for (int j = 0; j + 1 < NH; ++j) {
-        pcur[j][0] = pcur[j + 1][0];
-        pcur[j][1] = pcur[j + 1][1];
-      }
-    }
-    if (!SP && active) {
-      //   S = Q K^T, dP = dO V^T   (lane owns key `mykey`, 16 query rows)
-      //   P = exp2(s*scale*log2e - LSE2), dS = P (dP - D)
-      //   dV^T += dO^T P,  dK^T += Q^T dS
-      f32x16 sacc, pacc;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        sacc[r] = 0.f;
-        pacc[r] = 0.f;
-      }
-      // fragments of step kk+1 are read before the MFMAs of step kk; the Q
-      // and dO reads are a lane register plus a constant, the V read's address
-      // is added right before it (kept there: holding eight V addresses
-      // through the loop does not fit the register budget)
-      auto rdq = [&](int kk) {
-        return as_half8(*reinterpret_cast<const u32x4*>(smem + SM::Q_OFF + cur * SM::TQ +
-                                                        hq * 32 * RT::ROWB + rlane[kk]));
-      };
-      auto rdo = [&](int kk) {
-        return as_half8(*reinterpret_cast<const u32x4*>(smem + SM::DO_OFF + cur * SM::TQ +
-                                                        hq * 32 * RT::ROWB + rlane[kk]));
-      };
-      auto rdv = [&](int kk) {
-        uint32_t a;
-        asm volatile("v_add_u32 %0, %1, %2" : "=v"(a) : "v"(rlane[kk]), "s"(vrow0));
-        return as_half8(*reinterpret_cast<const u32x4*>(smem + a));
-      };
-      half8 fq = rdq(0);
-      half8 fd = rdo(0);
-      half8 fv = rdv(0);
-      __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        half8 nq = fq, nd = fd, nv = fv;
-        if (kk + 1 < KK) {
-          nq = rdq(kk + 1);
-          nd = rdo(kk + 1);
-          nv = rdv(kk + 1);
-        }
-        sacc = mfma32(fq, kf[kk], sacc);
-        pacc = mfma32(fd, fv, pacc);
-        if (kk + 1 < KK) {
-          __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);   // the three reads
-          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // then the two MFMAs
-        }
-        fq = nq;
-        fd = nd;
-        fv = nv;
-      }
-
-      __builtin_amdgcn_s_setprio(0);
-      float p[16], ds[16];
-#pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        const int ql0 = hq * 32 + 8 * rq + 4 * g;
-        const float4 l4 = *reinterpret_cast<const float4*>(lse_s + ql0);
-        const float4 d4 = *reinterpret_cast<const float4*>(del_s + ql0);
-        const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-        const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = 4 * rq + e;
-          p[r] = fast_exp2(fmaf(sacc[r], c, -lv[e]));
-          ds[r] = pacc[r] - dv[e];
-        }
-      }
-      if ((causal && kw0 + 31 > qh) || kw0 + 32 > S) {   // wave-uniform
-        // key > query (causal) or key past S -> P = 0
-        const int qlim = causal ? mykey : 0;
+      if (!SP && active) {
+        //   S = Q K^T, dP = dO V^T   (lane owns key `mykey`, 16 query rows)
+        //   P = exp2(s*scale*log2e - LSE2), dS = P (dP - D)
+        //   dV^T += dO^T P,  dK^T += Q^T dS
+        f32x16 sacc, pacc;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int q = qh + 8 * (r >> 2) + 4 * g + (r & 3);
-          p[r] = ((q < qlim) | (mykey >= S)) ? 0.f : p[r];
+          sacc[r] = 0.f;
+          pacc[r] = 0.f;
         }
-      }
+        // fragments of step kk+1 are read before the MFMAs of step kk; the Q
+        // and dO reads are a lane register plus a constant, the V read's address
+        // is added right before it (kept there: holding eight V addresses
+        // through the loop does not fit the register budget)
+        auto rdq = [&](int kk) {
+          return as_half8(*reinterpret_cast<const u32x4*>(smem + SM::Q_OFF + cur * SM::TQ +
+                                                          hq * 32 * RT::ROWB + rlane[kk]));
+        };
+        auto rdo = [&](int kk) {
+          return as_half8(*reinterpret_cast<const u32x4*>(smem + SM::DO_OFF + cur * SM::TQ +
+                                                          hq * 32 * RT::ROWB + rlane[kk]));
+        };
+        auto rdv = [&](int kk) {
+          uint32_t a;
+          asm volatile("v_add_u32 %0, %1, %2" : "=v"(a) : "v"(rlane[kk]), "s"(vrow0));
+          return as_half8(*reinterpret_cast<const u32x4*>(smem + a));
+        };
+        half8 fq = rdq(0);
+        half8 fd = rdo(0);
+        half8 fv = rdv(0);
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) ds[r] *= p[r];
-      half8 pp[2], pds[2];
-#pragma unroll
-      for (int kc = 0; kc < 2; ++kc) {
-        pp[kc] = pack8(p[8 * kc], p[8 * kc + 1], p[8 * kc + 2], p[8 * kc + 3], p[8 * kc + 4],
-                       p[8 * kc + 5], p[8 * kc + 6], p[8 * kc + 7]);
-        pds[kc] = pack8(ds[8 * kc], ds[8 * kc + 1], ds[8 * kc + 2], ds[8 * kc + 3],
-                        ds[8 * kc + 4], ds[8 * kc + 5], ds[8 * kc + 6], ds[8 * kc + 7]);
-      }
-      // dS block (query group qh / 32, key group kw0 / 32) for the dQ pass, as
-      // held here (lane-major, 32 bytes per lane).  The padded second half of
-      // a last query block lies past the sequence and is not stored.
-      if (qh < S) {
-        const int qg = qh >> 5;
-        const int kgi = kw0 >> 5;
-        const int64_t blk = causal ? (int64_t)qg * (qg + 1) / 2 + kgi
-                                   : (int64_t)qg * ((S + 31) >> 5) + kgi;
-        char* dst = reinterpret_cast<char*>(ds_out) +
-                    (((int64_t)b * Hq + h) * nblk + blk) * kDsBlockBytes + lane * 32;
-        // written once, read once by the dQ pass: non-temporal, so that the
-        // 2 KiB blocks (0.5 GB per call at S = 4096) do not evict the Q / dO
-        // blocks and K / V tiles the key tiles share through L2
-        __builtin_nontemporal_store(as_u32x4(pds[0]), reinterpret_cast<u32x4*>(dst));
-        __builtin_nontemporal_store(as_u32x4(pds[1]), reinterpret_cast<u32x4*>(dst + 16));
-      }
-      __builtin_amdgcn_s_setprio(1);
-      // steps (kc, db): the transposed dO and Q fragments of step s + 1 are
-      // read before step s's two MFMAs, into the other of two register sets
-      constexpr int NST = 2 * DB;
-      half8 tdo[2], tq[2];
-      auto rd_tr = [&](int st_, half8& a, half8& b) {
-        const int kc = st_ / DB, db = st_ % DB;
-        a = RT::template tr_frag<true>(dos, hq * 32 + kc * 16, db * 32, lane);
-        b = RT::template tr_frag<true>(qs, hq * 32 + kc * 16, db * 32, lane);
-      };
-      rd_tr(0, tdo[0], tq[0]);
-#pragma unroll
-      for (int st_ = 0; st_ < NST; ++st_) {
-        const int kc = st_ / DB, db = st_ % DB;
-        if (st_ + 1 < NST) rd_tr(st_ + 1, tdo[(st_ + 1) & 1], tq[(st_ + 1) & 1]);
-        dvacc[db] = mfma32(tdo[st_ & 1], pp[kc], dvacc[db]);
-        dkacc[db] = mfma32(tq[st_ & 1], pds[kc], dkacc[db]);
-        // the groups count from the top of the block: the first read group
-        // holds steps 0 and 1 (two transposed reads per fragment)
-        if (st_ + 1 < NST) {
-          if (st_ == 0)
-            __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
-          else
-            __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        for (int kk = 0; kk < KK; ++kk) {
+          half8 nq = fq, nd = fd, nv = fv;
+          if (kk + 1 < KK) {
+            nq = rdq(kk + 1);
+            nd = rdo(kk + 1);
+            nv = rdv(kk + 1);
+          }
+          sacc = mfma32(fq, kf[kk], sacc);
+          pacc = mfma32(fd, fv, pacc);
+          if (kk + 1 < KK) {
+            __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);   // the three reads
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // then the two MFMAs
+          }
+          fq = nq;
+          fd = nd;
+          fv = nv;
         }
+
+        __builtin_amdgcn_s_setprio(0);
+        float p[16], ds[16];
+#pragma unroll
+        for (int rq = 0; rq < 4; ++rq) {
+          const int ql0 = hq * 32 + 8 * rq + 4 * g;
+          const float4 l4 = *reinterpret_cast<const float4*>(lse_s + ql0);
+          const float4 d4 = *reinterpret_cast<const float4*>(del_s + ql0);
+          const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
+          const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int r = 4 * rq + e;
+            p[r] = fast_exp2(fmaf(sacc[r], c, -lv[e]));
+            ds[r] = pacc[r] - dv[e];
+          }
+        }
+        if ((causal && kw0 + 31 > qh) || kw0 + 32 > S) {   // wave-uniform
+          // key > query (causal) or key past S -> P = 0
+          const int qlim = causal ? mykey : 0;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int q = qh + 8 * (r >> 2) + 4 * g + (r & 3);
+            p[r] = ((q < qlim) | (mykey >= S)) ? 0.f : p[r];
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) ds[r] *= p[r];
+        half8 pp[2], pds[2];
+#pragma unroll
+        for (int kc = 0; kc < 2; ++kc) {
+          pp[kc] = pack8(p[8 * kc], p[8 * kc + 1], p[8 * kc + 2], p[8 * kc + 3], p[8 * kc + 4],
+                         p[8 * kc + 5], p[8 * kc + 6], p[8 * kc + 7]);
+          pds[kc] = pack8(ds[8 * kc], ds[8 * kc + 1], ds[8 * kc + 2], ds[8 * kc + 3],
+                          ds[8 * kc + 4], ds[8 * kc + 5], ds[8 * kc + 6], ds[8 * kc + 7]);
+        }
+        // dS block (query group qh / 32, key group kw0 / 32) for the dQ pass, as
+        // held here (lane-major, 32 bytes per lane).  The padded second half of
+        // a last query block lies past the sequence and is not stored.
+        if (qh < S) {
+          const int qg = qh >> 5;
+          const int kgi = kw0 >> 5;
+          const int64_t blk = causal ? (int64_t)qg * (qg + 1) / 2 + kgi
+                                     : (int64_t)qg * ((S + 31) >> 5) + kgi;
+          char* dst = reinterpret_cast<char*>(ds_out) +
+                      (((int64_t)b * Hq + h) * nblk + blk) * kDsBlockBytes + lane * 32;
+          // written once, read once by the dQ pass: non-temporal, so that the
+          // 2 KiB blocks (0.5 GB per call at S = 4096) do not evict the Q / dO
+          // blocks and K / V tiles the key tiles share through L2
+          __builtin_nontemporal_store(as_u32x4(pds[0]), reinterpret_cast<u32x4*>(dst));
+          __builtin_nontemporal_store(as_u32x4(pds[1]), reinterpret_cast<u32x4*>(dst + 16));
+        }
+        __builtin_amdgcn_s_setprio(1);
+        // steps (kc, db): the transposed dO and Q fragments of step s + 1 are
+        // read before step s's two MFMAs, into the other of two register sets
+        constexpr int NST = 2 * DB;
+        half8 tdo[2], tq[2];
+        auto rd_tr = [&](int st_, half8& a, half8& b) {
+          const int kc = st_ / DB, db = st_ % DB;
+          a = RT::template tr_frag<true>(dos, hq * 32 + kc * 16, db * 32, lane);
+          b = RT::template tr_frag<true>(qs, hq * 32 + kc * 16, db * 32, lane);
+        };
+        rd_tr(0, tdo[0], tq[0]);
+#pragma unroll
+        for (int st_ = 0; st_ < NST; ++st_) {
+          const int kc = st_ / DB, db = st_ % DB;
+          if (st_ + 1 < NST) rd_tr(st_ + 1, tdo[(st_ + 1) & 1], tq[(st_ + 1) & 1]);
+          dvacc[db] = mfma32(tdo[st_ & 1], pp[kc], dvacc[db]);
+          dkacc[db] = mfma32(tq[st_ & 1], pds[kc], dkacc[db]);
+          // the groups count from the top of the block: the first read group
+          // holds steps 0 and 1 (two transposed reads per fragment)
+          if (st_ + 1 < NST) {
+            if (st_ == 0)
+              __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+            else
+              __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+          }
+        }
+        __builtin_amdgcn_s_setprio(0);
       }
-      __builtin_amdgcn_s_setprio(0);
-    }
     };
     if constexpr (KSPLIT == 1 && !SP) {
 #pragma unroll
