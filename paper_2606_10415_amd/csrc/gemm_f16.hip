@@ -6,9 +6,15 @@
 // (DDR -> GSM -> SM / AM staging, VLIW micro-kernel) is replaced here by the
 // CDNA4 form of the same idea:
 //   * a workgroup owns a BM x BN output tile held in MFMA accumulators
-//     (16x16x32 FP16 MFMA, FP32 accumulate); 256x256 tiles use 8 waves, two
-//     per SIMD, so that one wave's LDS / barrier waits are covered by the
-//     other's MFMAs;
+//     (16x16x32 FP16 MFMA, FP32 accumulate).  256x256 tiles of the forward
+//     and data-gradient layouts use 4 waves, one per SIMD, each a 128x128
+//     wave tile with its accumulators in AGPRs; their main loop is a fixed
+//     sequence of asm statements (fragment reads a whole k-step ahead, MFMAs,
+//     direct loads, counter waits), so that one wave keeps its matrix unit
+//     fed without a second wave to cover its waits.  The weight-gradient
+//     layout (both operands read transposed) and the split-K partial tiles
+//     use 8 waves, two per SIMD, whose compiler-scheduled loop relies on the
+//     other wave to cover LDS and barrier waits;
 //   * K is walked in 64-wide slices, double-buffered in LDS.  Operands move
 //     HBM -> LDS with direct buffer loads (16 B per lane, no register
 //     staging), issued one slice ahead so that they overlap the current
@@ -37,6 +43,7 @@
 //   way as a whole when the split gives twice the workgroups of 128x128 tiles
 //   or keeps a long K loop per split; else it runs as 128x128 tiles.
 #include <type_traits>
+#include <utility>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -56,7 +63,7 @@ namespace {
 //       16-lane group, groups 8 k-rows apart) then hit every bank once.
 // Both are filled by direct global -> LDS loads issued as opaque
 // instructions, so the caller orders them with explicit vmcnt waits.
-template <int R, int BK, bool KC, int NT, bool PAIRED = false>
+template <int R, int BK, bool KC, int NT, bool PAIRED = false, int PB = 32>
 struct Operand {
   static constexpr int BYTES = R * BK * 2;
   static constexpr int NINST = BYTES / 1024;        // 1 KiB direct loads per slice
@@ -94,8 +101,8 @@ struct Operand {
 #pragma unroll
       for (int t = 0; t < PERW; ++t) {
         const int r = (wave * PERW + t) * RPI + lane / CPR;
-        const int64_t idx = row0 + 32 * (r >> 6) + (r & 31);
-        const int64_t abs_row = idx + ((r >> 5) & 1 ? pair_off : 0);
+        const int64_t idx = row0 + PB * (r / (2 * PB)) + (r % PB);
+        const int64_t abs_row = idx + ((r / PB) & 1 ? pair_off : 0);
         const int c = (lane % CPR) ^ swz(r);
         voff[t] = idx < rows ? (uint32_t)((abs_row * ld + c * 8) * 2) : kOOB;
       }
@@ -163,6 +170,37 @@ struct Operand {
     }
   }
 
+  // buffer descriptor of the full K-contiguous slice at k0 (uniform)
+  __device__ __forceinline__ u32x4 desc(int64_t k0) const {
+    const uint64_t b = (uint64_t)(!KC ? base + k0 * ld + row0 : PAIRED ? base + k0 : base + row0 * ld + k0);
+    u32x4 r;
+    r[0] = __builtin_amdgcn_readfirstlane((uint32_t)b);
+    r[1] = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32) & 0xffffu);
+    r[2] = __builtin_amdgcn_readfirstlane(!KC || PAIRED ? nrec : nrec - (uint32_t)(k0 * 2));
+    r[3] = 0x00020000u;
+    return r;
+  }
+
+  // one direct load (index t of this wave's PERW) of the K-contiguous slice
+  // at k0 with kv = clamp(K - k0, 0, BK) valid columns; kv = 0 fills the
+  // tile with zeros and touches no memory (empty range)
+  __device__ __forceinline__ void load1(char* lds, int64_t k0, int kv, int t, int wave,
+                                        int lane) const {
+    const int i = wave * PERW + t;
+    if constexpr (KC) {
+      const lt_half* b = PAIRED ? base + (kv > 0 ? k0 : 0) : base + row0 * ld + (kv > 0 ? k0 : 0);
+      const uint32_t n = kv > 0 ? (PAIRED ? nrec : nrec - (uint32_t)(k0 * 2)) : 0u;
+      const int r = i * RPI + lane / CPR;
+      const uint32_t off = ((lane % CPR) ^ swz(r)) * 8 >= kv ? kOOB : voff[t];
+      lds_dma16_opaque(b, n, lds + i * 1024, off);
+    } else {
+      const lt_half* b = base + (kv > 0 ? k0 * ld : 0) + row0;
+      const uint32_t n = kv > 0 ? nrec : 0u;
+      const uint32_t off = i * KR_PER + lane / LPR >= kv ? kOOB : voff[t];
+      lds_dma16_opaque(b, n, lds + i * 1024, off);
+    }
+  }
+
   // K % 8 != 0 (K-contiguous tiles only; the k-major layout loads whole
   // k-rows, so its rows past K are already zero): the chunk of each row that
   // straddles K was loaded whole and holds the row's next elements in memory
@@ -226,6 +264,78 @@ __device__ __forceinline__ void wait_slices(int n) {
   }
 }
 
+// ---- building blocks of the 4-wave main loop ----
+// The loop is written as asm statements that the compiler keeps in program
+// order (volatile asm).  Two rules make that safe with the compiler still
+// allocating the registers:
+//   * a fragment read issued by asm is, to the compiler, complete at once; its
+//     registers must not be read, copied or reused before the explicit
+//     lgkmcnt wait.  Every fragment is consumed only by MFMA asm after that
+//     wait (xfence re-defines the two halves of a transposed fragment after
+//     the wait, so that joining them happens there), and the fragments read
+//     for a step that never runs are kept allocated until the final wait
+//     (xkeep);
+//   * MFMAs issued by asm are not seen by the compiler's hazard checks: the
+//     wait states before any other instruction reads an accumulator are in
+//     one statement that takes every accumulator as an operand.
+template <int... I, class F>
+__device__ __forceinline__ void sfor_impl(std::integer_sequence<int, I...>, F&& f) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void sfor(F&& f) {
+  sfor_impl(std::make_integer_sequence<int, N>{}, f);
+}
+// direct 16-byte-per-lane load into LDS at m0 = mbase + OFF (uniform)
+template <int OFF>
+__device__ __forceinline__ void dma16_at(uint32_t mbase, uint32_t voff, u32x4 desc) {
+  asm volatile("s_add_u32 m0, %0, %3\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(mbase), "v"(voff), "s"(desc), "n"(OFF)
+               : "memory");
+}
+// LDS transpose read of one half of a k-major fragment
+template <int OFF>
+__device__ __forceinline__ void xrd_tr(u32x2& d, uint32_t a) {
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(d) : "v"(a), "n"(OFF));
+}
+// the two halves are (re)defined here: nothing that joins them moves above
+__device__ __forceinline__ void xfence(u32x2& a, u32x2& b) {
+  asm volatile("" : "+v"(a), "+v"(b));
+}
+// keep a value's registers allocated up to this point
+__device__ __forceinline__ void xkeep(const half8& a) { asm volatile("" ::"v"(a)); }
+__device__ __forceinline__ void xkeep(const u32x2& a, const u32x2& b) { asm volatile("" ::"v"(a), "v"(b)); }
+// read q of a 4-wave step: fragments in the order B0, A0, B1..B7, A1..A7,
+// ra (rb) reads per A (B) fragment; op 0 = A, 1 = B
+struct X4Rd {
+  int op, f, h;
+};
+constexpr X4Rd x4_read(int q, int ra, int rb) {
+  for (int e = 0; e < 16; ++e) {
+    const int op = e == 0 ? 1 : e == 1 ? 0 : e <= 8 ? 1 : 0;
+    const int f = e <= 1 ? 0 : e <= 8 ? e - 1 : e - 8;
+    const int n = op ? rb : ra;
+    if (q < n) return X4Rd{op, f, q};
+    q -= n;
+  }
+  return X4Rd{-1, 0, 0};
+}
+// reads issued after MFMA idx of a step: [x4_q0(idx), x4_q0(idx + 1))
+constexpr int x4_q0(int idx, int nrd) {
+  const int q = idx < 2 ? 0 : ((idx - 2) * nrd + 47) / 48;
+  return q < nrd ? q : nrd;
+}
+// LDS read of a K-contiguous fragment
+template <int OFF>
+__device__ __forceinline__ void xrd(half8& d, uint32_t a) {
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(d) : "v"(a), "n"(OFF));
+}
+// c += a b (16x16x32), c in AGPRs
+__device__ __forceinline__ void xmma(f32x4& c, const half8& a, const half8& b) {
+  asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
+}
+
 __device__ __forceinline__ float sigmoid_f(float x) { return 1.f / (1.f + __expf(-x)); }
 
 template <int BM, int BN, int WGM, int WGN, int BK, int NS, bool TA, bool TB, int EPI,
@@ -240,7 +350,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   constexpr int NT = WGM * WGN * kWave;
   constexpr int WTM = BM / WGM, WTN = BN / WGN;   // wave tile
   constexpr int TM = WTM / 16, TN = WTN / 16;     // 16x16 MFMA blocks per wave
-  static_assert(EPI != 1 || (TB && WTN == 64), "paired gate/up tiles: 32 + 32 columns per wave");
+  static_assert(EPI != 1 || TB, "paired gate/up tiles: K-contiguous weights");
   // Loader waves: in an 8-wave tile only waves 0-3 (one per SIMD) issue the
   // direct loads, twice as many each; the other four waves only compute.
   // Fewer waves feeding the shared load queues measured 4-13% faster in
@@ -249,7 +359,8 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   constexpr int LOADERS = NWAVE >= 8 ? 4 : NWAVE;
   constexpr bool SPLIT_ISSUE = LOADERS < NWAVE;
   using OA = Operand<BM, BK, !TA, LOADERS * kWave>;
-  using OB = Operand<BN, BK, TB, LOADERS * kWave, EPI == 1>;
+  // EPI 1: a wave's columns are WTN/2 gate rows and the same WTN/2 up rows
+  using OB = Operand<BN, BK, TB, LOADERS * kWave, EPI == 1, WTN / 2>;
   constexpr int STAGE = OA::BYTES + OB::BYTES;
   constexpr int PER_SLICE = OA::PERW + OB::PERW;  // direct loads per wave per slice
   static_assert(NS >= 2 && (NS - 1) * PER_SLICE <= 63, "vmcnt range");
@@ -334,6 +445,193 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   };
   constexpr bool ragged_k = KFIX;
 
+  constexpr bool X4 = NT == 256 && BM == 256 && BN == 256 && EPI <= 2 && !RK && BK == 64 && NS == 2 &&
+                     !(TA && !TB);
+  if constexpr (X4) {
+    // One wave per SIMD, 128x128 wave tiles, accumulators in AGPRs.  Every
+    // fragment read, MFMA and counter wait of the loop is an ordered asm
+    // statement: a step's MFMAs run on one register set while the reads of
+    // the next step fill the other, all issued in the step's first 48 MFMAs;
+    // after the slice barrier the 16 direct loads of slice kt+2 are spread
+    // over the step's MFMAs.
+    static_assert(TM == 8 && TN == 8 && STAGE == 65536 && OA::BYTES == 32768, "X4 shape");
+    constexpr bool AK = !TA, BKC = TB;           // K-contiguous operands (row reads)
+    constexpr int XRA = AK ? 1 : 2, XRB = BKC ? 1 : 2;
+    constexpr int NRD = 8 * (XRA + XRB);        // LDS reads per step
+    half8 xa[2][8], xb[2][8];                  // fragments of K-contiguous operands
+    u32x2 ta[2][8][2], tb[2][8][2];            // ... of k-major ones (two transpose reads)
+    const uint32_t sbase = (uint32_t)(uintptr_t)smem;
+    // K-contiguous: fragment f of k-step kk at r[stage][kk] + 2048 f
+    auto lterm = [&](int kk) {
+      const int r = lane & 15;
+      const int c = kk * 4 + (lane >> 4);
+      return (uint32_t)(r * 128 + ((c ^ (r >> 1)) << 4));
+    };
+    // k-major: read h of fragment f, k-step kk at z[stage][f] + 16384 kk + 2048 h
+    // (the fragment's XOR-swizzled position differs per lane only in address
+    // bits 5..7, which no other term touches)
+    auto yterm = [&](int wx) {
+      const int kl = (lane >> 2) & 3, g1 = (lane >> 4) & 1;
+      return (uint32_t)(((8 * (lane >> 4) + kl) * 512 + 256 * wx + 16 * ((lane & 3) >> 1) + 8 * (lane & 1)) |
+                        (kl << 6) | (g1 << 5));
+    };
+    uint32_t ra[2][2], rb[2][2], za[2][8], zb[2][8];
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        ra[p][kk] = sbase + p * STAGE + wm * 16384 + lterm(kk);
+        rb[p][kk] = sbase + p * STAGE + OA::BYTES + wn * 16384 + lterm(kk);
+      }
+#pragma unroll
+      for (int f = 0; f < 8; ++f) {
+        const uint32_t cf = ((f >> 1) << 6) | ((f & 1) << 5);
+        za[p][f] = (sbase + p * STAGE + yterm(wm)) ^ cf;
+        zb[p][f] = (sbase + p * STAGE + OA::BYTES + yterm(wn)) ^ cf;
+      }
+    }
+    // read q of the step into set D, from stage P, k-step KK
+    auto xread = [&](auto Q_, auto D_, auto P_, auto KK_) {
+      constexpr X4Rd r = x4_read(decltype(Q_)::value, XRA, XRB);
+      constexpr int D = decltype(D_)::value, P = decltype(P_)::value, KK = decltype(KK_)::value;
+      if constexpr (r.op == 0) {
+        if constexpr (AK) xrd<r.f * 2048>(xa[D][r.f], ra[P][KK]);
+        else xrd_tr<KK * 16384 + r.h * 2048>(ta[D][r.f][r.h], za[P][r.f]);
+      } else {
+        if constexpr (BKC) xrd<r.f * 2048>(xb[D][r.f], rb[P][KK]);
+        else xrd_tr<KK * 16384 + r.h * 2048>(tb[D][r.f][r.h], zb[P][r.f]);
+      }
+    };
+    // set S resident: wait for its reads; the k-major halves are joined
+    // only after the wait
+    auto xwait = [&](auto S_) {
+      constexpr int S = decltype(S_)::value;
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+      for (int f = 0; f < 8; ++f) {
+        if constexpr (!AK) xfence(ta[S][f][0], ta[S][f][1]);
+        if constexpr (!BKC) xfence(tb[S][f][0], tb[S][f][1]);
+      }
+    };
+    auto fragA = [&](auto S_, int i) {
+      constexpr int S = decltype(S_)::value;
+      if constexpr (AK) return xa[S][i];
+      else return __builtin_bit_cast(half8, __builtin_shufflevector(ta[S][i][0], ta[S][i][1], 0, 1, 2, 3));
+    };
+    auto fragB = [&](auto S_, int j) {
+      constexpr int S = decltype(S_)::value;
+      if constexpr (BKC) return xb[S][j];
+      else return __builtin_bit_cast(half8, __builtin_shufflevector(tb[S][j][0], tb[S][j][1], 0, 1, 2, 3));
+    };
+    using Z0 = std::integral_constant<int, 0>;
+    using Z1 = std::integral_constant<int, 1>;
+    // prologue: slices 0 and 1 in flight, slice 0 resident, its first
+    // k-step's fragments into set 0
+    auto kv_of = [&](int kt) {
+      const int64_t rem = K - (int64_t)kt * BK;
+      return rem >= BK ? BK : rem > 0 ? (int)rem : 0;
+    };
+#pragma unroll
+    for (int sl = 0; sl < NS; ++sl)
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        oa.load1(smem + sl * STAGE, (int64_t)sl * BK, kv_of(sl), t, wave, lane);
+        ob.load1(smem + sl * STAGE + OA::BYTES, (int64_t)sl * BK, kv_of(sl), t, wave, lane);
+      }
+    asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+    __syncthreads();
+    sfor<NRD>([&](auto Q) { xread(Q, Z0{}, Z0{}, Z0{}); });
+    const uint32_t mbase = __builtin_amdgcn_readfirstlane(sbase + wave * 8 * 1024);
+    // One 32-wide k-step on set S; the next step's fragments come from
+    // stage P, k-step KK.  LD: 0 no loads, 1 loads of any slice at lk0 (lkv
+    // valid columns, masked) into the stage at lst, 2 loads of a full slice
+    // through the descriptors dA, dB into stage LP.
+    auto xstep = [&](auto S_, auto P_, auto KK_, auto LD_, char* lst, int64_t lk0, int lkv,
+                     auto LP_, u32x4 dA, u32x4 dB) {
+      constexpr int S = decltype(S_)::value;
+      constexpr int LD = decltype(LD_)::value;
+      constexpr int LP = decltype(LP_)::value;
+      xwait(S_);
+      sfor<64>([&](auto IDX) {
+        constexpr int idx = decltype(IDX)::value;
+        constexpr int i = idx / 8, j = idx % 8;
+        xmma(acc[i][j], fragB(S_, j), fragA(S_, i));
+        constexpr int q0 = x4_q0(idx, NRD), q1 = x4_q0(idx + 1, NRD);
+        static_assert(q1 - q0 <= 2, "at most two reads per MFMA");
+        sfor<2>([&](auto R_) {
+          constexpr int q = q0 + decltype(R_)::value;
+          if constexpr (q < q1) xread(std::integral_constant<int, q>{}, std::integral_constant<int, S ^ 1>{}, P_, KK_);
+        });
+        if constexpr (LD == 1 && idx % 4 == 1) {
+          constexpr int t = idx / 4;
+          if constexpr (t < 8) oa.load1(lst, lk0, lkv, t, wave, lane);
+          else ob.load1(lst + OA::BYTES, lk0, lkv, t - 8, wave, lane);
+        }
+        if constexpr (LD == 2 && idx % 4 == 1) {
+          constexpr int t = idx / 4;
+          if constexpr (t < 8) dma16_at<LP * STAGE + t * 1024>(mbase, oa.voff[t], dA);
+          else dma16_at<LP * STAGE + OA::BYTES + (t - 8) * 1024>(mbase, ob.voff[t - 8], dB);
+        }
+      });
+    };
+    using NO = std::integral_constant<int, 0>;
+    using YS = std::integral_constant<int, 1>;
+    using FS = std::integral_constant<int, 2>;
+    const u32x4 dz = {0, 0, 0, 0};
+    // Slices are taken in pairs (stage 0, stage 1).  For an odd slice count
+    // the last pair's second slice lies past K: its stage was filled with
+    // zeros, so its products add exact zeros (an accumulator that starts at
+    // +0 never holds -0), and the loop body has no branch.
+    auto xslice = [&](int kt, auto P_, auto FAST_) {
+      constexpr int P = decltype(P_)::value;
+      constexpr bool FAST = decltype(FAST_)::value;
+      xstep(Z0{}, P_, Z1{}, NO{}, nullptr, 0, 0, P_, dz, dz);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      __syncthreads();
+      const int64_t lk0 = (int64_t)(kt + 2) * BK;
+      if constexpr (FAST)
+        xstep(Z1{}, std::integral_constant<int, P ^ 1>{}, Z0{}, FS{}, nullptr, 0, 0, P_,
+              oa.desc(lk0), ob.desc(lk0));
+      else
+        xstep(Z1{}, std::integral_constant<int, P ^ 1>{}, Z0{}, YS{}, smem + P * STAGE, lk0,
+              kv_of(kt + 2), P_, dz, dz);
+    };
+    // pairs whose loads (slices kt+2, kt+3) are whole slices inside K take
+    // the unmasked loads
+    const int nkf = (int)(K / BK);
+    int kt = 0;
+    for (; kt + 3 < nkf; kt += 2) {
+      xslice(kt, Z0{}, std::true_type{});
+      xslice(kt + 1, Z1{}, std::true_type{});
+    }
+    for (; kt < nk; kt += 2) {
+      xslice(kt, Z0{}, std::false_type{});
+      xslice(kt + 1, Z1{}, std::false_type{});
+    }
+    // The last step read the fragments of a step that never runs: their
+    // registers stay allocated until those reads have landed, so that no
+    // epilogue value is placed where a late LDS result would overwrite it.
+    // The MFMAs are opaque to the compiler's hazard checks: the wait states
+    // before the accumulators may be read sit in one statement that takes
+    // every accumulator, so no spill or copy of one can be placed between
+    // the last MFMA and the wait.
+#define X4_ROW(i) "+a"(acc[i][0]), "+a"(acc[i][1]), "+a"(acc[i][2]), "+a"(acc[i][3]), \
+                  "+a"(acc[i][4]), "+a"(acc[i][5]), "+a"(acc[i][6]), "+a"(acc[i][7])
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7\n\t"
+                 "s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7"
+                 : X4_ROW(0), X4_ROW(1), X4_ROW(2), X4_ROW(3), X4_ROW(4), X4_ROW(5), X4_ROW(6), X4_ROW(7)
+                 :
+                 : "memory");
+#undef X4_ROW
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+      if constexpr (AK) xkeep(xa[0][f]);
+      else xkeep(ta[0][f][0], ta[0][f][1]);
+      if constexpr (BKC) xkeep(xb[0][f]);
+      else xkeep(tb[0][f][0], tb[0][f][1]);
+    }
+  } else {
   // Fragments: A in place (each re-read right after its last use), B
   // double-buffered (used by every A row of a step).
   half8 fa[TM], fb[2][TN];
@@ -444,6 +742,8 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
       }
     });
   }
+
+  }  // !X4
 
   // ---- epilogue ----
   // lane holds column m = ... + lane % 16 and rows n = ... + 4*(lane/16) + 0..3
@@ -621,6 +921,14 @@ template <int BM, int BN, int WGM, int WGN, int BK, int NS, bool TA, bool TB, in
 hipError_t launch(const GemmArgs& g, hipStream_t s, int splits = 1) {
   const int tiles_m = (int)((g.M + BM - 1) / BM);
   const int tiles_n = EPI == 1 ? (int)((g.F + BN / 2 - 1) / (BN / 2)) : (int)((g.N + BN - 1) / BN);
+  if constexpr (BM == 256 && BN == 256 && WGM == 2 && WGN == 4 && EPI <= 2 && !RK && BK == 64 && NS == 2 &&
+                !(TA && !TB)) {
+    hipLaunchKernelGGL((gemm_f16_kernel<256, 256, 2, 2, 64, 2, TA, TB, EPI, false>),
+                       dim3(tiles_m * tiles_n, splits), dim3(4 * kWave), 0, s, g.M, g.N, g.K, g.alpha,
+                       g.A, g.lda, g.B, g.ldb, g.beta, g.R, g.ldr, g.C, g.ldc, tiles_m, tiles_n, 8,
+                       g.X1, g.ldx1, g.F, g.pair_off > 0 ? g.pair_off : g.F, g.bias);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL((gemm_f16_kernel<BM, BN, WGM, WGN, BK, NS, TA, TB, EPI, RK>),
                      dim3(tiles_m * tiles_n, splits), dim3(WGM * WGN * kWave), 0, s, g.M, g.N, g.K, g.alpha,
                      g.A, g.lda, g.B, g.ldb, g.beta, g.R, g.ldr, g.C, g.ldc, tiles_m, tiles_n, 8,
