@@ -45,9 +45,9 @@ GEMM_TRAFFIC = {
     "workload": "llama2-7b",
     "layer": "paper",
     "fuse_swiglu": True,
-    "sources_sha256": "980fbbb9e74475907d8dd9f0ef2443a73e59870bfbf7691b3ea679014a45e9bf",
-    "fetch_bytes_per_launch": 664285414,
-    "write_bytes_per_launch": 99802084,
+    "sources_sha256": "b0e7034e46238bb3d4197960ac97e553a8e6768512e4a22e45147f80fa2a61d6",
+    "fetch_bytes_per_launch": 667385255,
+    "write_bytes_per_launch": 105554320,
 }
 GEMM_SOURCES = ("paper_2606_10415_amd/csrc/gemm_f16.hip", "paper_2606_10415_amd/csrc/common.hpp",
                 "paper_2606_10415_amd/csrc/plan.cpp")
