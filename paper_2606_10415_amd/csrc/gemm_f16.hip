@@ -445,8 +445,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   };
   constexpr bool ragged_k = KFIX;
 
-  constexpr bool X4 = NT == 256 && BM == 256 && BN == 256 && EPI <= 2 && !RK && BK == 64 && NS == 2 &&
-                     !(TA && !TB);
+  constexpr bool X4 = NT == 256 && BM == 256 && BN == 256 && EPI <= 2 && !RK && BK == 64 && NS == 2;
   if constexpr (X4) {
     // One wave per SIMD, 128x128 wave tiles, accumulators in AGPRs.  Every
     // fragment read, MFMA and counter wait of the loop is an ordered asm
@@ -491,7 +490,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
       }
     }
     // read q of the step into set D, from stage P, k-step KK
-    auto xread = [&](auto Q_, auto D_, auto P_, auto KK_) {
+    auto xread = [&](auto Q_, auto D_, auto P_, auto KK_) __attribute__((always_inline)) {
       constexpr X4Rd r = x4_read(decltype(Q_)::value, XRA, XRB);
       constexpr int D = decltype(D_)::value, P = decltype(P_)::value, KK = decltype(KK_)::value;
       if constexpr (r.op == 0) {
@@ -504,7 +503,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
     };
     // set S resident: wait for its reads; the k-major halves are joined
     // only after the wait
-    auto xwait = [&](auto S_) {
+    auto xwait = [&](auto S_) __attribute__((always_inline)) {
       constexpr int S = decltype(S_)::value;
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
@@ -513,12 +512,12 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
         if constexpr (!BKC) xfence(tb[S][f][0], tb[S][f][1]);
       }
     };
-    auto fragA = [&](auto S_, int i) {
+    auto fragA = [&](auto S_, int i) __attribute__((always_inline)) {
       constexpr int S = decltype(S_)::value;
       if constexpr (AK) return xa[S][i];
       else return __builtin_bit_cast(half8, __builtin_shufflevector(ta[S][i][0], ta[S][i][1], 0, 1, 2, 3));
     };
-    auto fragB = [&](auto S_, int j) {
+    auto fragB = [&](auto S_, int j) __attribute__((always_inline)) {
       constexpr int S = decltype(S_)::value;
       if constexpr (BKC) return xb[S][j];
       else return __builtin_bit_cast(half8, __builtin_shufflevector(tb[S][j][0], tb[S][j][1], 0, 1, 2, 3));
@@ -540,25 +539,25 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
       }
     asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
     __syncthreads();
-    sfor<NRD>([&](auto Q) { xread(Q, Z0{}, Z0{}, Z0{}); });
+    sfor<NRD>([&](auto Q) __attribute__((always_inline)) { xread(Q, Z0{}, Z0{}, Z0{}); });
     const uint32_t mbase = __builtin_amdgcn_readfirstlane(sbase + wave * 8 * 1024);
     // One 32-wide k-step on set S; the next step's fragments come from
     // stage P, k-step KK.  LD: 0 no loads, 1 loads of any slice at lk0 (lkv
     // valid columns, masked) into the stage at lst, 2 loads of a full slice
     // through the descriptors dA, dB into stage LP.
     auto xstep = [&](auto S_, auto P_, auto KK_, auto LD_, char* lst, int64_t lk0, int lkv,
-                     auto LP_, u32x4 dA, u32x4 dB) {
+                     auto LP_, u32x4 dA, u32x4 dB) __attribute__((always_inline)) {
       constexpr int S = decltype(S_)::value;
       constexpr int LD = decltype(LD_)::value;
       constexpr int LP = decltype(LP_)::value;
       xwait(S_);
-      sfor<64>([&](auto IDX) {
+      sfor<64>([&](auto IDX) __attribute__((always_inline)) {
         constexpr int idx = decltype(IDX)::value;
         constexpr int i = idx / 8, j = idx % 8;
         xmma(acc[i][j], fragB(S_, j), fragA(S_, i));
         constexpr int q0 = x4_q0(idx, NRD), q1 = x4_q0(idx + 1, NRD);
         static_assert(q1 - q0 <= 2, "at most two reads per MFMA");
-        sfor<2>([&](auto R_) {
+        sfor<2>([&](auto R_) __attribute__((always_inline)) {
           constexpr int q = q0 + decltype(R_)::value;
           if constexpr (q < q1) xread(std::integral_constant<int, q>{}, std::integral_constant<int, S ^ 1>{}, P_, KK_);
         });
@@ -582,7 +581,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
     // the last pair's second slice lies past K: its stage was filled with
     // zeros, so its products add exact zeros (an accumulator that starts at
     // +0 never holds -0), and the loop body has no branch.
-    auto xslice = [&](int kt, auto P_, auto FAST_) {
+    auto xslice = [&](int kt, auto P_, auto FAST_) __attribute__((always_inline)) {
       constexpr int P = decltype(P_)::value;
       constexpr bool FAST = decltype(FAST_)::value;
       xstep(Z0{}, P_, Z1{}, NO{}, nullptr, 0, 0, P_, dz, dz);
@@ -921,8 +920,7 @@ template <int BM, int BN, int WGM, int WGN, int BK, int NS, bool TA, bool TB, in
 hipError_t launch(const GemmArgs& g, hipStream_t s, int splits = 1) {
   const int tiles_m = (int)((g.M + BM - 1) / BM);
   const int tiles_n = EPI == 1 ? (int)((g.F + BN / 2 - 1) / (BN / 2)) : (int)((g.N + BN - 1) / BN);
-  if constexpr (BM == 256 && BN == 256 && WGM == 2 && WGN == 4 && EPI <= 2 && !RK && BK == 64 && NS == 2 &&
-                !(TA && !TB)) {
+  if constexpr (BM == 256 && BN == 256 && WGM == 2 && WGN == 4 && EPI <= 2 && !RK && BK == 64 && NS == 2) {
     hipLaunchKernelGGL((gemm_f16_kernel<256, 256, 2, 2, 64, 2, TA, TB, EPI, false>),
                        dim3(tiles_m * tiles_n, splits), dim3(4 * kWave), 0, s, g.M, g.N, g.K, g.alpha,
                        g.A, g.lda, g.B, g.ldb, g.beta, g.R, g.ldr, g.C, g.ldc, tiles_m, tiles_n, 8,
