@@ -45,9 +45,9 @@ GEMM_TRAFFIC = {
     "workload": "llama2-7b",
     "layer": "paper",
     "fuse_swiglu": True,
-    "sources_sha256": "b0e7034e46238bb3d4197960ac97e553a8e6768512e4a22e45147f80fa2a61d6",
-    "fetch_bytes_per_launch": 667385255,
-    "write_bytes_per_launch": 105554320,
+    "sources_sha256": "0fccf47c32c77ad618d74245511d528afc77dd1079c172ecda280b2585c0f8ed",
+    "fetch_bytes_per_launch": 680459595,
+    "write_bytes_per_launch": 107861722,
 }
 GEMM_SOURCES = ("paper_2606_10415_amd/csrc/gemm_f16.hip", "paper_2606_10415_amd/csrc/common.hpp",
                 "paper_2606_10415_amd/csrc/plan.cpp")
