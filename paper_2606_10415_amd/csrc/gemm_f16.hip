@@ -11,10 +11,10 @@
 //     wave tile with its accumulators in AGPRs; their main loop is a fixed
 //     sequence of asm statements (fragment reads a whole k-step ahead, MFMAs,
 //     direct loads, counter waits), so that one wave keeps its matrix unit
-//     fed without a second wave to cover its waits.  The weight-gradient
-//     layout (both operands read transposed) and the split-K partial tiles
-//     use 8 waves, two per SIMD, whose compiler-scheduled loop relies on the
-//     other wave to cover LDS and barrier waits;
+//     fed without a second wave to cover its waits.  Every layout and the
+//     split-K partial tiles use it; the half-size tail tiles and the
+//     ragged-K form use 8 waves, two per SIMD, whose compiler-scheduled loop
+//     relies on the other wave to cover LDS and barrier waits;
 //   * K is walked in 64-wide slices, double-buffered in LDS.  Operands move
 //     HBM -> LDS with direct buffer loads (16 B per lane, no register
 //     staging), issued one slice ahead so that they overlap the current
@@ -445,7 +445,7 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
   };
   constexpr bool ragged_k = KFIX;
 
-  constexpr bool X4 = NT == 256 && BM == 256 && BN == 256 && EPI <= 2 && !RK && BK == 64 && NS == 2;
+  constexpr bool X4 = NT == 256 && BM == 256 && BN == 256 && EPI <= 3 && !RK && BK == 64 && NS == 2;
   if constexpr (X4) {
     // One wave per SIMD, 128x128 wave tiles, accumulators in AGPRs.  Every
     // fragment read, MFMA and counter wait of the loop is an ordered asm
@@ -920,7 +920,7 @@ template <int BM, int BN, int WGM, int WGN, int BK, int NS, bool TA, bool TB, in
 hipError_t launch(const GemmArgs& g, hipStream_t s, int splits = 1) {
   const int tiles_m = (int)((g.M + BM - 1) / BM);
   const int tiles_n = EPI == 1 ? (int)((g.F + BN / 2 - 1) / (BN / 2)) : (int)((g.N + BN - 1) / BN);
-  if constexpr (BM == 256 && BN == 256 && WGM == 2 && WGN == 4 && EPI <= 2 && !RK && BK == 64 && NS == 2) {
+  if constexpr (BM == 256 && BN == 256 && WGM == 2 && WGN == 4 && EPI <= 3 && !RK && BK == 64 && NS == 2) {
     hipLaunchKernelGGL((gemm_f16_kernel<256, 256, 2, 2, 64, 2, TA, TB, EPI, false>),
                        dim3(tiles_m * tiles_n, splits), dim3(4 * kWave), 0, s, g.M, g.N, g.K, g.alpha,
                        g.A, g.lda, g.B, g.ldb, g.beta, g.R, g.ldr, g.C, g.ldc, tiles_m, tiles_n, 8,
