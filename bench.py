@@ -45,9 +45,9 @@ GEMM_TRAFFIC = {
     "workload": "llama2-7b",
     "layer": "paper",
     "fuse_swiglu": True,
-    "sources_sha256": "0fccf47c32c77ad618d74245511d528afc77dd1079c172ecda280b2585c0f8ed",
-    "fetch_bytes_per_launch": 680459595,
-    "write_bytes_per_launch": 107861722,
+    "sources_sha256": "96e73fb8eed04fe8ebffa94d869405c09bf7affcb7944bc8f9e3ba70b3dc101a",
+    "fetch_bytes_per_launch": 675613934,
+    "write_bytes_per_launch": 107849960,
 }
 GEMM_SOURCES = ("paper_2606_10415_amd/csrc/gemm_f16.hip", "paper_2606_10415_amd/csrc/common.hpp",
                 "paper_2606_10415_amd/csrc/plan.cpp")
