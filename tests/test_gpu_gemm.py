@@ -71,6 +71,26 @@ def test_gemm_exact_integers_bitwise(env, transA, transB, M, N, K):
 
 
 @pytest.mark.parametrize("transA,transB", LAYOUTS)
+@pytest.mark.parametrize("M,N,K", [
+    # >= 192 whole-wave 256x256 tiles: the 4-wave loop, whose 64-wide slices
+    # run in pairs (an odd count adds a zero-filled slice) and whose unmasked
+    # loads serve only slices inside K
+    (4096, 3072, 320),    # 5 slices (odd), all whole
+    (4000, 3112, 4104),   # 65 slices, the last 8 wide; M and N tails
+    (3848, 3328, 200),    # 4 slices, the last 8 wide; M and N tails
+    (4096, 3072, 8),      # a single 8-wide slice
+])
+def test_gemm_four_wave_slices_exact_integers_bitwise(env, transA, transB, M, N, K):
+    print(f"gemm 4-wave slices trans=({transA},{transB}) M={M} N={N} K={K}", flush=True)
+    a = uniform_int_f16(31, (M, K), -2, 2)
+    b = uniform_int_f16(32, (K, N), -2, 2)
+    c = uniform_int_f16(33, (M, N), -8, 8)
+    got = _run(env, transA, transB, M, N, K, 3.0, a, b, -2.0, c)
+    ref = oracle.gemm(0, 0, 3.0, a, b, -2.0, c).astype(np.float16)
+    assert np.array_equal(got.view(np.uint16), ref.view(np.uint16))
+
+
+@pytest.mark.parametrize("transA,transB", LAYOUTS)
 def test_gemm_residual_operand_bitwise(env, transA, transB):
     M, N, K = 200, 136, 264
     a = uniform_int_f16(4, (M, K), -2, 2)
