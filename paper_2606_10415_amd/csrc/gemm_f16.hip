@@ -555,6 +555,13 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
         constexpr int idx = decltype(IDX)::value;
         constexpr int i = idx / 8, j = idx % 8;
         xmma(acc[i][j], fragB(S_, j), fragA(S_, i));
+        // the slice barrier after the second step's first two MFMAs (they
+        // run on registers and cover the barrier's skew): slice kt+1
+        // resident for every wave, and nobody reads slice kt's stage any more
+        if constexpr (S == 1 && idx == 1) {
+          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+          __syncthreads();
+        }
         constexpr int q0 = x4_q0(idx, NRD), q1 = x4_q0(idx + 1, NRD);
         static_assert(q1 - q0 <= 2, "at most two reads per MFMA");
         sfor<2>([&](auto R_) __attribute__((always_inline)) {
@@ -585,9 +592,6 @@ gemm_f16_kernel(int64_t M, int64_t N, int64_t K, float alpha,
       constexpr int P = decltype(P_)::value;
       constexpr bool FAST = decltype(FAST_)::value;
       xstep(Z0{}, P_, Z1{}, NO{}, nullptr, 0, 0, P_, dz, dz);
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-      __syncthreads();
       const int64_t lk0 = (int64_t)(kt + 2) * BK;
       if constexpr (FAST)
         xstep(Z1{}, std::integral_constant<int, P ^ 1>{}, Z0{}, FS{}, nullptr, 0, 0, P_,
