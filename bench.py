@@ -45,9 +45,9 @@ GEMM_TRAFFIC = {
     "workload": "llama2-7b",
     "layer": "paper",
     "fuse_swiglu": True,
-    "sources_sha256": "96e73fb8eed04fe8ebffa94d869405c09bf7affcb7944bc8f9e3ba70b3dc101a",
-    "fetch_bytes_per_launch": 675613934,
-    "write_bytes_per_launch": 107849960,
+    "sources_sha256": "28b551bfcc85b63f527c7da3ddeff34891f1f5593ab9b9fe949b55c495b6b5ce",
+    "fetch_bytes_per_launch": 675429221,
+    "write_bytes_per_launch": 108471157,
 }
 GEMM_SOURCES = ("paper_2606_10415_amd/csrc/gemm_f16.hip", "paper_2606_10415_amd/csrc/common.hpp",
                 "paper_2606_10415_amd/csrc/plan.cpp")
